@@ -1,0 +1,348 @@
+"""Pins of the oracle against things other than itself: published test
+vectors, library routines, closed forms, invariants and brute force. CPU only.
+
+A plausible mistake anywhere in the oracle (a dropped term, a wrong sign or
+index, a transposed operand) should fail at least one of these.
+"""
+
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from oracle import decode as od
+from oracle import kvalloc as ka
+from oracle.schedule import was_schedule
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- bf16 storage
+
+def test_bf16_roundtrip_and_rne():
+    # Every bf16 pattern survives bits -> f64 -> bits (finite and inf).
+    bits = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
+    vals = od.bf16_bits_to_f64(bits)
+    finite = ~np.isnan(vals)
+    assert np.array_equal(od.f64_to_bf16_bits(vals[finite]), bits[finite])
+    # torch's own float32 -> bfloat16 conversion (round to nearest even) as the judge.
+    x = np.random.default_rng(0).standard_normal(100_000).astype(np.float32) * 37.0
+    x = np.concatenate([x, np.float32([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -8, 65504.0, 3.0e38])])
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(od.f64_to_bf16_bits(x.astype(np.float64)), ref)
+
+
+# ---------------------------------------------------------------- per-op pins
+
+def test_rms_norm_matches_torch_library():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5, 96)) * 3.0
+    g = 1.0 + 0.1 * rng.standard_normal(96)
+    ref = F.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps=1e-5).numpy()
+    np.testing.assert_allclose(od.rms_norm(x, g, 1e-5), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_rms_norm_closed_form_constant_vector():
+    c, eps = 0.37, 1e-6
+    y = od.rms_norm(np.full((1, 64), c), np.full(64, 2.0), eps)
+    np.testing.assert_allclose(y, 2.0 * c / math.sqrt(c * c + eps), rtol=1e-15)
+
+
+def test_silu_matches_torch_library():
+    z = np.linspace(-30, 30, 2001)
+    np.testing.assert_allclose(od.silu(z), F.silu(torch.from_numpy(z)).numpy(), rtol=1e-14, atol=1e-300)
+
+
+def _rope_complex(x, pos, theta):
+    """RoPE as complex multiplication: (x_i + i x_{i+D/2}) * exp(i pos theta_i)."""
+    D = x.shape[-1]
+    half = D // 2
+    z = x[..., :half] + 1j * x[..., half:]
+    freqs = theta ** (-np.arange(0, D, 2) / D)
+    z = z * np.exp(1j * pos * freqs)
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def test_rope_matches_complex_rotation():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((3, 128))
+    for pos in (0, 1, 17, 4095, 8192):
+        np.testing.assert_allclose(od.rope_rotate_half(x, np.full(3, pos), 500000.0),
+                                   _rope_complex(x, pos, 500000.0), rtol=1e-12, atol=1e-12)
+
+
+def test_rope_identity_norm_and_relative_position():
+    rng = np.random.default_rng(3)
+    q, k = rng.standard_normal(64), rng.standard_normal(64)
+    np.testing.assert_array_equal(od.rope_rotate_half(q[None], np.array([0]), 1e4)[0], q)
+    r = od.rope_rotate_half(q[None], np.array([123]), 1e4)[0]
+    # pairwise norms preserved
+    np.testing.assert_allclose(r[:32] ** 2 + r[32:] ** 2, q[:32] ** 2 + q[32:] ** 2, rtol=1e-12)
+    # q_m . k_n depends only on m - n
+    dots = [od.rope_rotate_half(q[None], np.array([m]), 1e4)[0] @ od.rope_rotate_half(k[None], np.array([m - 5]), 1e4)[0]
+            for m in (5, 40, 300)]
+    np.testing.assert_allclose(dots, dots[0], rtol=1e-11)
+
+
+def _paged_case(rng, Hq=8, Hkv=2, D=32, bs=16, nblk=12, seq=37):
+    k_cache = rng.standard_normal((nblk, Hkv, bs, D))
+    v_cache = rng.standard_normal((nblk, Hkv, bs, D))
+    table = rng.permutation(nblk)[: -(-seq // bs)]
+    q = rng.standard_normal((Hq, D))
+    return q, k_cache, v_cache, table
+
+
+def _gather(cache, table, seq, bs):
+    t = np.arange(seq)
+    return cache[np.asarray(table)[t // bs], :, t % bs, :]  # (seq, Hkv, D)
+
+
+def test_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(4)
+    for seq in (1, 15, 16, 17, 37):
+        q, kc, vc, tab = _paged_case(rng, seq=seq)
+        out = od.paged_gqa_attention(q, kc, vc, tab, seq, 16)
+        K = torch.from_numpy(_gather(kc, tab, seq, 16)).permute(1, 0, 2)  # (Hkv, seq, D)
+        V = torch.from_numpy(_gather(vc, tab, seq, 16)).permute(1, 0, 2)
+        ref = F.scaled_dot_product_attention(torch.from_numpy(q)[:, None, :], K.repeat_interleave(4, 0),
+                                             V.repeat_interleave(4, 0))[:, 0, :].numpy()
+        np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(5)
+    q, kc, vc, tab = _paged_case(rng, seq=1)
+    out = od.paged_gqa_attention(q, kc, vc, tab, 1, 16)
+    # one cached token: every head returns that token's V row of its group
+    for h in range(8):
+        np.testing.assert_array_equal(out[h], vc[tab[0], h // 4, 0, :])
+    # all-equal keys: the mean of V
+    q, kc, vc, tab = _paged_case(rng, seq=29)
+    kc[:] = rng.standard_normal(32)
+    out = od.paged_gqa_attention(q, kc, vc, tab, 29, 16)
+    Vg = _gather(vc, tab, 29, 16)
+    for h in range(8):
+        np.testing.assert_allclose(out[h], Vg[:, h // 4, :].mean(axis=0), rtol=1e-12, atol=1e-14)
+
+
+def test_attention_softmax_rows_sum_to_one():
+    # V = 1 everywhere -> output is the row sum of the softmax, i.e. 1
+    rng = np.random.default_rng(6)
+    q, kc, vc, tab = _paged_case(rng, seq=40)
+    q *= 10.0
+    out = od.paged_gqa_attention(q, kc, np.ones_like(vc), tab, 40, 16)
+    np.testing.assert_allclose(out, 1.0, rtol=1e-12)
+
+
+def test_attention_physical_block_permutation_invariance():
+    rng = np.random.default_rng(7)
+    q, kc, vc, tab = _paged_case(rng, seq=45, nblk=10)
+    out1 = od.paged_gqa_attention(q, kc, vc, tab, 45, 16)
+    perm = rng.permutation(10)  # move every physical block elsewhere
+    kc2, vc2 = np.empty_like(kc), np.empty_like(vc)
+    kc2[perm], vc2[perm] = kc, vc
+    out2 = od.paged_gqa_attention(q, kc2, vc2, perm[tab], 45, 16)
+    np.testing.assert_array_equal(out1, out2)
+
+
+# ---------------------------------------------------------------- block tables
+
+def _golden_splitmix():
+    rows = {}
+    with open(os.path.join(GOLDEN, "splitmix64_vectors.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            seed, vals = line.split(":")
+            rows[int(seed)] = [int(v) for v in vals.split()]
+    return rows
+
+
+def test_splitmix64_published_vectors():
+    for seed, vals in _golden_splitmix().items():
+        assert ka.splitmix64_stream(seed, len(vals)) == vals
+
+
+def test_fisher_yates_is_uniform_permutation():
+    # Durstenfeld's rule j = r mod (i+1) reaches every permutation; the
+    # off-by-one j = r mod i (Sattolo) would only reach the 2 cyclic ones of 3.
+    seen = {}
+    for seed in range(3000):
+        p = tuple(ka.fisher_yates(3, seed))
+        seen[p] = seen.get(p, 0) + 1
+    assert len(seen) == 6
+    counts = np.array(list(seen.values()))
+    chi2 = ((counts - 500.0) ** 2 / 500.0).sum()
+    assert chi2 < 20.5  # 5 dof, p ~ 0.001
+    for n in (1, 2, 64, 1000):
+        assert sorted(ka.fisher_yates(n, 11)) == list(range(n))
+
+
+def test_block_tables_properties():
+    ctx = [16, 17, 0, 63, 64, 31]
+    tabs = ka.allocate_block_tables(ctx, 1, 64, 6, seed=3)
+    used = []
+    for c, row in zip(ctx, tabs):
+        need = -(-(c + 1) // 16)
+        assert all(b >= 0 for b in row[:need]) and all(b == -1 for b in row[need:])
+        used += row[:need]
+    assert len(used) == len(set(used)) and all(0 <= b < 64 for b in used)
+    # the blocks are handed out in permutation order
+    assert used == ka.fisher_yates(64, 3)[:len(used)]
+    # exhaustion and table-width overflow are refused
+    assert ka.allocate_block_tables([500], 1, 16, 64, seed=0) is None
+    assert ka.allocate_block_tables([100], 1, 64, 4, seed=0) is None
+
+
+def test_slot_mapping_brute_force():
+    # Enumerate every token of every sequence; slots must be distinct and
+    # land in the block the table names, at the token's offset.
+    ctx = [5, 33, 48]
+    tabs = ka.allocate_block_tables(ctx, 1, 20, 4, seed=9)
+    slots = set()
+    for c, row in zip(ctx, tabs):
+        for p in range(c + 1):
+            s = ka.slot_of(row, p)
+            assert s // 16 == row[p // 16] and s % 16 == p % 16
+            slots.add(s)
+    assert len(slots) == sum(c + 1 for c in ctx)
+
+
+# ---------------------------------------------------------------- schedule
+
+def test_was_schedule_ordering():
+    L, steps, n = 5, 3, 2
+    copy_ops, comp_ops = was_schedule(L, steps, n)
+    total = L * steps
+    fills = [g for (op, g, s) in copy_ops if op == "fill"]
+    assert fills == list(range(total + n))  # always n layers ahead
+    for (op, g, s) in copy_ops + comp_ops:
+        assert s == g % n
+    # compute g waits its own fill; fill g+n waits compute g's done
+    assert [g for (op, g, s) in comp_ops if op == "wait_fill"] == list(range(total))
+    for i, (op, g, s) in enumerate(copy_ops):
+        if op == "fill" and g >= n:
+            assert copy_ops[i - 1] == ("wait_done", g - n, s)
+    # at most n layers resident: between wait_done(g) and fill(g+n) no other fill to s
+    assert was_schedule(L, 0, n) == ([], [])
+
+
+# ---------------------------------------------------------------- whole layer
+
+def _tiny_inputs(cfg, seed=0, gains="random"):
+    w = synth.layer_weights(cfg, 0, seed=seed, gains=gains)
+    lw = {k: v.view(torch.int16).numpy().view(np.uint16) for k, v in w.items()}
+    ctx = synth.context_lengths(cfg, seed)
+    tabs = np.array(ka.allocate_block_tables(ctx, 1, cfg["num_phys_blocks"], 5, seed))
+    kb, vb = synth.kv_prefill(cfg, cfg["num_phys_blocks"], 0, seed)
+    kc = od.bf16_bits_to_f64(kb.view(torch.int16).numpy().view(np.uint16))
+    vc = od.bf16_bits_to_f64(vb.view(torch.int16).numpy().view(np.uint16))
+    x = synth.hidden_input(cfg, seed).double().numpy()
+    return w, lw, ctx, tabs, kc, vc, x
+
+
+def _hf_layer(family, cfg, w):
+    if family == "llama":
+        from transformers import LlamaConfig as C
+        from transformers.models.llama.modeling_llama import LlamaDecoderLayer as Layer, LlamaRotaryEmbedding as Rot
+    elif family == "qwen2":
+        from transformers import Qwen2Config as C
+        from transformers.models.qwen2.modeling_qwen2 import Qwen2DecoderLayer as Layer, Qwen2RotaryEmbedding as Rot
+    else:
+        from transformers import Qwen3Config as C
+        from transformers.models.qwen3.modeling_qwen3 import Qwen3DecoderLayer as Layer, Qwen3RotaryEmbedding as Rot
+    hc = C(hidden_size=cfg["hidden"], intermediate_size=cfg["ffn_dim"], num_attention_heads=cfg["num_q_heads"],
+           num_key_value_heads=cfg["num_kv_heads"], head_dim=cfg["head_dim"], rms_norm_eps=cfg["rms_eps"],
+           rope_theta=cfg["rope_theta"], max_position_embeddings=8192, attn_implementation="eager",
+           num_hidden_layers=1)
+    layer = Layer(hc, layer_idx=0).to(torch.float64).eval()
+    sd = lambda t: t.to(torch.float64)  # noqa: E731
+    with torch.no_grad():
+        a = layer.self_attn
+        a.q_proj.weight.copy_(sd(w["w_q"]))
+        a.k_proj.weight.copy_(sd(w["w_k"]))
+        a.v_proj.weight.copy_(sd(w["w_v"]))
+        a.o_proj.weight.copy_(sd(w["w_o"]))
+        if family == "qwen2":
+            a.q_proj.bias.copy_(sd(w["b_q"]))
+            a.k_proj.bias.copy_(sd(w["b_k"]))
+            a.v_proj.bias.copy_(sd(w["b_v"]))
+        if family == "qwen3":
+            a.q_norm.weight.copy_(sd(w["g_q"]))
+            a.k_norm.weight.copy_(sd(w["g_k"]))
+        layer.mlp.gate_proj.weight.copy_(sd(w["w_gate"]))
+        layer.mlp.up_proj.weight.copy_(sd(w["w_up"]))
+        layer.mlp.down_proj.weight.copy_(sd(w["w_down"]))
+        layer.input_layernorm.weight.copy_(sd(w["g_attn"]))
+        layer.post_attention_layernorm.weight.copy_(sd(w["g_mlp"]))
+    return layer, Rot(hc).to(torch.float64)
+
+
+@pytest.mark.parametrize("family", ["llama", "qwen2", "qwen3"])
+def test_decode_layer_matches_transformers(family):
+    """The whole layer against the public model-family implementation
+    (transformers, float64, eager attention) driven through one decode step
+    with a cache prefilled from the paged blocks."""
+    from transformers import DynamicCache
+    cfg = synth.get_config("tiny_layer", qkv_bias=int(family == "qwen2"), qk_norm=int(family == "qwen3"),
+                           rms_eps=1e-5 if family == "llama" else 1e-6)
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    kc0, vc0 = kc.copy(), vc.copy()
+    out = od.decode_layer(x, lw, cfg, kc, vc, ctx, tabs, round_bf16=False)
+    layer, rot = _hf_layer(family, cfg, w)
+    for b in range(cfg["batch"]):
+        c = int(ctx[b])
+        K = torch.from_numpy(_gather(kc0, tabs[b], c, 16)).permute(1, 0, 2)[None]  # (1, Hkv, c, D)
+        V = torch.from_numpy(_gather(vc0, tabs[b], c, 16)).permute(1, 0, 2)[None]
+        cache = DynamicCache()
+        cache.update(K.clone(), V.clone(), 0)
+        hs = torch.from_numpy(x[b])[None, None]
+        pid = torch.tensor([[c]])
+        with torch.no_grad():
+            y = layer(hs, attention_mask=None, position_ids=pid, past_key_values=cache, use_cache=True,
+                      position_embeddings=rot(hs, pid))
+        y = y[0] if isinstance(y, tuple) else y
+        np.testing.assert_allclose(out[b], y[0, 0].numpy(), rtol=2e-5, atol=2e-5)
+        # the cache row written for the new token equals what transformers appended
+        k_new = kc[tabs[b][c // 16], :, c % 16, :]
+        np.testing.assert_allclose(k_new, cache.layers[0].keys[0, :, c, :].numpy(), rtol=2e-5, atol=2e-5)
+
+
+def test_decode_layer_zero_projections_keep_residual_and_write_kv():
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    lw["w_o"] = np.zeros_like(lw["w_o"])
+    lw["w_down"] = np.zeros_like(lw["w_down"])
+    kc0 = kc.copy()
+    cfg2 = dict(cfg, num_layers=3)
+    out = od.decode_stack(x, [lw] * 3, cfg2, [kc], [vc], ctx, tabs)
+    np.testing.assert_array_equal(out, x)
+    changed = np.argwhere(np.any(kc != kc0, axis=(1, 3)))
+    expect = {(int(tabs[b][c // 16]), int(c % 16)) for b, c in enumerate(ctx)}
+    got = {(int(r[0]), int(r[2])) for r in np.argwhere(np.any(kc != kc0, axis=-1))}
+    assert got == expect and len(changed) > 0
+
+
+def test_decode_layer_rows_independent():
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    full = od.decode_layer(x, lw, cfg, kc.copy(), vc.copy(), ctx, tabs)
+    for b in (0, 5):
+        one = od.decode_layer(x[b:b + 1], lw, cfg, kc.copy(), vc.copy(), ctx[b:b + 1], tabs[b:b + 1])
+        np.testing.assert_array_equal(one[0], full[b])
+
+
+def test_bf16_mode_close_to_exact_mode():
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    a = od.decode_layer(x, lw, cfg, kc.copy(), vc.copy(), ctx, tabs, round_bf16=True)
+    b = od.decode_layer(x, lw, cfg, kc.copy(), vc.copy(), ctx, tabs, round_bf16=False)
+    rel = np.max(np.abs(a - b), axis=1) / np.max(np.abs(b), axis=1)
+    assert rel.max() < 5e-3
+    assert np.any(a != b)
