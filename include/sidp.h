@@ -1,0 +1,240 @@
+/*
+ * sidp.h - C ABI of the MI355X Weight-as-a-Service decode step.
+ *
+ * One GPU's share of SiDP's Weight-as-a-Service mode (arXiv 2605.28095):
+ * every layer's weights live in a pool, are copied layer by layer into a ring
+ * of two pre-allocated cache slots on a side stream, and the batch's decode
+ * tokens run through the layer from its slot while the next layer is being
+ * fetched (§4.2 "Asynchronous one-sided reading", "Asynchronous buffer
+ * management"; §4.4 "Implementation"). On one GPU the owner's pool is a second
+ * region of the same HBM.
+ *
+ * The layer is a dense decoder block (§2.1): RMSNorm, fused QKV projection
+ * (optional bias), optional per-head QK RMSNorm, rotary embedding, append of
+ * the new token's key/value to a paged KV cache, grouped-query attention
+ * decode, output projection with residual, RMSNorm, gate/up projection with
+ * SwiGLU, down projection with residual. One new token per sequence per call
+ * (§2.2).
+ *
+ * Conventions for every entry point:
+ *  - Return value: SIDP_OK (0) or a negative SIDP_E* code; no exceptions or
+ *    aborts cross the ABI. sidp_strerror() names a code.
+ *  - "device" pointers are HIP device memory of the current device; "host"
+ *    pointers are ordinary host memory. The caller owns every buffer it
+ *    passes; the library never frees caller memory and keeps pointers given
+ *    to sidp_pool_init / sidp_kv_attach until sidp_destroy.
+ *  - Streams are hipStream_t values passed as void* (NULL = null stream).
+ *    Work is enqueued asynchronously; device-side input errors (a position
+ *    outside its block table, a block index out of range) are latched in the
+ *    handle and reported by sidp_sync.
+ *  - bf16 is IEEE bfloat16 stored as 16-bit words; rounding from fp32 is
+ *    round-to-nearest-even.
+ *  - After SIDP_EHIP a handle is poisoned: later calls return SIDP_ESTATE.
+ *  - One handle per host thread; calls on one handle are not thread-safe.
+ */
+#ifndef SIDP_H
+#define SIDP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---- */
+#define SIDP_OK          0
+#define SIDP_EINVAL     (-1) /* bad argument, unsupported shape, or bad device-side input */
+#define SIDP_ENOBLOCKS  (-2) /* paged-KV blocks or block-table width exhausted */
+#define SIDP_ESTATE     (-3) /* call out of order, or handle poisoned */
+#define SIDP_EHIP       (-4) /* a HIP runtime call failed (sidp_last_hip_error) */
+#define SIDP_ENOMEM     (-5) /* library-owned device memory could not be allocated */
+
+/* ---- sidp_decode_step flags ---- */
+#define SIDP_RESIDENT      0x0  /* each layer computes straight from its pool blob */
+#define SIDP_STREAMED      0x1  /* layers stream through the 2-slot cache ring */
+#define SIDP_COPY_MEMCPY   0x2  /* slot fills by hipMemcpyAsync (default: library copy kernel) */
+#define SIDP_DEBUG_POISON  0x10 /* before each fill, write NaN bytes over the slot */
+#define SIDP_DEBUG_DELAY   0x20 /* before each fill, spin ~200 us on the copy stream */
+
+/* ---- sidp_linear epilogues ---- */
+#define SIDP_EPI_BF16    0 /* out bf16 [m, n] = x W^T (+ bias)                      */
+#define SIDP_EPI_RESID   1 /* out fp32 [m, n] = residual + x W^T (may alias residual) */
+#define SIDP_EPI_SWIGLU  2 /* out bf16 [m, f] = silu(x Wg^T) * (x Wu^T), W from sidp_pack_gate_up */
+
+typedef struct sidp_handle sidp_handle;
+
+/* Model shape and limits. All counts > 0 unless stated. */
+typedef struct sidp_config {
+  int32_t num_layers;    /* L, layers in the stack                                  */
+  int32_t hidden;        /* H, multiple of 64                                        */
+  int32_t num_q_heads;   /* Hq                                                       */
+  int32_t num_kv_heads;  /* Hkv; Hq % Hkv == 0 and Hq / Hkv <= 16                   */
+  int32_t head_dim;      /* D: 64 or 128                                             */
+  int32_t ffn_dim;       /* F, multiple of 16                                        */
+  int32_t qkv_bias;      /* 1: QKV projection has a bias (Qwen2.5 family)            */
+  int32_t qk_norm;       /* 1: per-head RMSNorm on q and k before RoPE (Qwen3 family) */
+  int32_t block_size;    /* paged-KV tokens per block; must be 16                    */
+  int32_t max_batch;     /* largest batch any call will use (sizes scratch)          */
+  int32_t max_seq_len;   /* largest position + 1 any call will use (RoPE table)      */
+  float rms_eps;         /* RMSNorm epsilon (inside the square root)                 */
+  float qk_norm_eps;     /* epsilon of the per-head QK RMSNorm                       */
+  float rope_theta;      /* RoPE base; rotate-half pairing (i, i + D/2)              */
+} sidp_config;
+
+/* One layer's weights, device pointers to bf16 arrays in nn.Linear layout
+ * [out_features, in_features], row-major. Bias and QK-norm pointers are read
+ * only when the config enables them (else may be NULL). */
+typedef struct sidp_layer_weights {
+  const void *w_q;    /* [Hq*D, H]  */
+  const void *w_k;    /* [Hkv*D, H] */
+  const void *w_v;    /* [Hkv*D, H] */
+  const void *w_o;    /* [H, Hq*D]  */
+  const void *w_gate; /* [F, H]     */
+  const void *w_up;   /* [F, H]     */
+  const void *w_down; /* [H, F]     */
+  const void *b_q, *b_k, *b_v; /* [Hq*D], [Hkv*D], [Hkv*D] */
+  const void *g_attn; /* [H] RMSNorm gain before attention */
+  const void *g_mlp;  /* [H] RMSNorm gain before the FFN   */
+  const void *g_q, *g_k; /* [D] per-head QK RMSNorm gains  */
+} sidp_layer_weights;
+
+/* ---- errors ---- */
+const char *sidp_strerror(int code);
+/* The hipError_t value behind the last SIDP_EHIP on this handle (0 if none). */
+int sidp_last_hip_error(const sidp_handle *h);
+
+/* ---- handle ----
+ * sidp_create validates the config (SIDP_EINVAL), binds the handle to the
+ * current HIP device, and allocates the library's own device memory:
+ * activations for max_batch rows, split-K and attention partials, the RoPE
+ * cos/sin table (max_seq_len x D/2, computed on the host in double precision
+ * and stored as fp32), the device error word and the fill/consume events of
+ * the slot ring. The slot ring is the paper's pre-allocated cache slots with
+ * completion notifications (§4.2 "Asynchronous buffer management", §4.4). */
+int sidp_create(const sidp_config *cfg, sidp_handle **out);
+/* Waits for the handle's outstanding work, frees what sidp_create allocated. */
+int sidp_destroy(sidp_handle *h);
+
+/* ---- weight pool and cache slots (§4.1 initialisation; §4.2; §4.4 slots) ----
+ * Bytes of one packed layer blob: the pool stride and the size of one slot.
+ * Returns 0 for an invalid config. */
+size_t sidp_layer_bytes(const sidp_config *cfg);
+/* Registers caller-owned device memory: `pool` holds num_layers blobs
+ * (pool_bytes >= L * sidp_layer_bytes), `slots` holds 2 slots
+ * (slots_bytes >= 2 * sidp_layer_bytes; may be NULL/0 if only
+ * SIDP_RESIDENT steps will run). Both must be 256-byte aligned. */
+int sidp_pool_init(sidp_handle *h, void *pool, size_t pool_bytes, void *slots, size_t slots_bytes);
+/* Packs one layer's weights (device pointers, layout above) into its pool
+ * blob: norm gains, QKV bias, then the QKV, O, interleaved gate/up and down
+ * matrices re-laid into the GEMM's fragment order. Asynchronous on `stream`;
+ * the sources may be freed once the stream has passed this call. */
+int sidp_pool_load_layer(sidp_handle *h, int32_t layer, const sidp_layer_weights *w, void *stream);
+
+/* ---- paged KV cache (per-request KV state, §2.2) ----
+ * Host-only (no GPU work): builds block tables. Physical blocks
+ * [0, num_phys_blocks) are handed out in the order of a Fisher-Yates
+ * (Durstenfeld) shuffle driven by splitmix64(seed); sequence b takes the next
+ * ceil((ctx_lens[b] + reserve_tokens) / block_size) of them as its logical
+ * blocks 0, 1, .... block_tables (host, [batch, max_blocks_per_seq], int32)
+ * receives them, padded with -1. Returns SIDP_ENOBLOCKS if the blocks or the
+ * table width do not suffice, SIDP_EINVAL for bad sizes. */
+int sidp_kv_alloc(int32_t batch, const int32_t *ctx_lens, int32_t reserve_tokens, int32_t block_size,
+                  int32_t num_phys_blocks, uint64_t seed, int32_t max_blocks_per_seq, int32_t *block_tables);
+/* Bytes of one KV region of the K cache (the V cache has the same size):
+ * num_phys_blocks * Hkv * block_size * D * 2. */
+size_t sidp_kv_region_bytes(const sidp_config *cfg, int32_t num_phys_blocks);
+/* Registers caller-owned KV caches of num_regions regions each. Layer l reads
+ * and writes region l % num_regions. Layouts (bf16):
+ *   K: [region][block][kv_head][token in block][d]
+ *   V: [region][block][kv_head][d][token in block]   (transposed per block)
+ * Cached keys are stored after RoPE (and after QK-norm when enabled). */
+int sidp_kv_attach(sidp_handle *h, void *k_cache, void *v_cache, int32_t num_phys_blocks, int32_t num_regions);
+
+/* ---- the decode step (§2.2 iteration; §4.2 WaS) ----
+ * Runs one decode iteration of all L layers for `batch` sequences.
+ *  hidden       device fp32 [batch, H], the residual stream: input token
+ *               states, overwritten with the last layer's output.
+ *  positions    device int32 [batch]: tokens already cached per sequence; the
+ *               new token's k, v are written at that position and attention
+ *               covers positions[b] + 1 keys. The caller advances positions.
+ *  block_tables device int32 [batch, max_blocks_per_seq] (from sidp_kv_alloc).
+ *  flags        SIDP_RESIDENT or SIDP_STREAMED, optionally | SIDP_COPY_MEMCPY
+ *               and the SIDP_DEBUG_* bits.
+ *  compute      stream for the layer kernels.
+ *  copy         stream for slot fills (STREAMED only; must differ from compute).
+ * STREAMED keeps a ring of 2 slots: layer g (counted across calls) computes
+ * from slot g % 2 after waiting for its fill; the fill of layer g + 2 waits
+ * for layer g's compute to release the slot. The copy stream thus runs two
+ * layers ahead, into the next call's first layers too. RESIDENT and STREAMED
+ * give bit-identical results (the paper's modes change only where weights
+ * live, §4.1). Returns without waiting for the GPU. */
+int sidp_decode_step(sidp_handle *h, float *hidden, const int32_t *positions, const int32_t *block_tables,
+                     int32_t max_blocks_per_seq, int32_t batch, int32_t flags, void *compute, void *copy);
+/* Waits for all work the handle enqueued on both streams; returns
+ * SIDP_EINVAL if a kernel latched a device-side input error since the last
+ * sync (and clears it), SIDP_EHIP on an asynchronous HIP error. */
+int sidp_sync(sidp_handle *h);
+
+/* ---- the slot-ring plan (host only) ----
+ * The order in which sidp_decode_step issues ring operations for `steps`
+ * streamed calls of num_layers layers, 2 slots. Each op is 3 int32
+ * {kind, global layer g, slot}; kinds: 0 fill, 1 wait-fill, 2 compute,
+ * 3 done, 4 wait-done. copy_ops/compute_ops receive up to *n_copy/*n_compute
+ * ops (host arrays of 3*capacity int32); on return the counts are the numbers
+ * of ops written. SIDP_EINVAL if a capacity is too small. */
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t *copy_ops, int32_t *n_copy,
+              int32_t *compute_ops, int32_t *n_compute);
+
+/* ---- single kernels, for parity checks and reuse ----
+ * All enqueue on `stream` and return immediately. */
+
+/* RMSNorm (K1/K6): out[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps) * gain).
+ * x device fp32 [rows, n]; gain device bf16 [n]; out device bf16 [rows, n];
+ * n multiple of 4. */
+int sidp_rmsnorm(const float *x, const void *gain, float eps, void *out, int32_t rows, int32_t n, void *stream);
+
+/* Bytes of a matrix [n, k] packed for sidp_linear (n padded to 64, k to 64). */
+size_t sidp_packed_bytes(int32_t n, int32_t k);
+/* Packs W (device bf16 [n, k], nn.Linear layout) into `packed`
+ * (device, sidp_packed_bytes(n, k) bytes, 256-byte aligned). */
+int sidp_pack_linear(const void *w, int32_t n, int32_t k, void *packed, void *stream);
+/* Packs gate and up (device bf16 [f, k] each) interleaved 32 rows at a time
+ * for SIDP_EPI_SWIGLU; `packed` needs sidp_packed_bytes(2 * f32, k) bytes
+ * where f32 = f rounded up to 32. */
+int sidp_pack_gate_up(const void *w_gate, const void *w_up, int32_t f, int32_t k, void *packed, void *stream);
+/* Dense projection on MFMA: x device bf16 [m, k] row-major times packed W^T.
+ * m <= max_batch of the handle; n = output columns (for SWIGLU: f).
+ * bias: device bf16 [n] or NULL (EPI_BF16 only); residual: device fp32 [m, n]
+ * (EPI_RESID only; may equal out). Uses the handle's split-K scratch. */
+int sidp_linear(sidp_handle *h, const void *x, int32_t m, int32_t k, const void *packed, int32_t n,
+                int32_t epilogue, const void *bias, const float *residual, void *out, void *stream);
+
+/* Slot mapping (K9): slots[b] = bt[b][p / bs] * bs + p % bs, p = positions[b];
+ * device int32 arrays. An entry out of range yields -1 and latches
+ * SIDP_EINVAL for sidp_sync. */
+int sidp_slot_mapping(sidp_handle *h, const int32_t *positions, const int32_t *block_tables,
+                      int32_t max_blocks_per_seq, int32_t batch, int32_t *slots, void *stream);
+/* QK-norm (when configured) + RoPE + KV append for one layer's KV region:
+ * qkv device bf16 [batch, (Hq + 2 Hkv) D] (q heads, then k heads, then v
+ * heads); q_out device bf16 [batch, Hq, D] receives the rotated queries; the
+ * rotated keys and the values are written into region `region` of the attached
+ * caches at each sequence's position. g_q/g_k: device bf16 [D] or NULL. */
+int sidp_rope_append(sidp_handle *h, const void *qkv, const int32_t *positions, const int32_t *block_tables,
+                     int32_t max_blocks_per_seq, int32_t batch, const void *g_q, const void *g_k,
+                     int32_t region, void *q_out, void *stream);
+/* Paged GQA decode attention (K4) over region `region`: for each sequence b
+ * and query head h, softmax(q K^T / sqrt(D)) V over tokens [0, positions[b]]
+ * of KV head h / (Hq / Hkv). q device bf16 [batch, Hq, D]; out device bf16
+ * [batch, Hq, D]. */
+int sidp_attention(sidp_handle *h, const void *q, int32_t region, const int32_t *positions,
+                   const int32_t *block_tables, int32_t max_blocks_per_seq, int32_t batch, void *out,
+                   void *stream);
+/* Device-to-device copy by the library's copy kernel (the slot-fill engine),
+ * using `grid` workgroups (0 = default). src, dst 16-byte aligned. */
+int sidp_copy(const void *src, void *dst, size_t bytes, int32_t grid, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SIDP_H */

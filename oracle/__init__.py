@@ -43,6 +43,8 @@ from .decode import (  # noqa: F401
     rms_norm,
     rope_rotate_half,
     silu,
+    linear,
+    swiglu,
     paged_gqa_attention,
     decode_layer,
     decode_stack,

@@ -81,6 +81,17 @@ def silu(z):
         return z / (1.0 + np.exp(-z))
 
 
+def linear(x, w, b=None):
+    """Dense projection in nn.Linear layout: x W^T (+ b)."""
+    y = np.asarray(x, dtype=np.float64) @ np.asarray(w, dtype=np.float64).T
+    return y if b is None else y + b
+
+
+def swiglu(h, w_gate, w_up):
+    """SwiGLU FFN input: silu(h W_gate^T) * (h W_up^T)."""
+    return silu(linear(h, w_gate)) * linear(h, w_up)
+
+
 def paged_gqa_attention(q, k_cache, v_cache, block_table, seq_len, block_size):
     """Decode attention of one sequence over its paged KV.
 
@@ -95,6 +106,8 @@ def paged_gqa_attention(q, k_cache, v_cache, block_table, seq_len, block_size):
     group = Hq // Hkv
     t = np.arange(seq_len)
     blocks = np.asarray(block_table)[t // block_size]
+    if np.any(blocks < 0):
+        raise ValueError("a token of the sequence lies in an unallocated block")
     offs = t % block_size
     K = k_cache[blocks, :, offs, :]  # (seq, Hkv, D)
     V = v_cache[blocks, :, offs, :]
@@ -142,13 +155,10 @@ def decode_layer(x, lw, cfg, k_cache, v_cache, positions, block_tables, round_bf
 
     # Self-attention sub-block.
     h = rb(rms_norm(x, _w(lw, "g_attn"), cfg["rms_eps"]))
-    q = h @ _w(lw, "w_q").T
-    k = h @ _w(lw, "w_k").T
-    v = h @ _w(lw, "w_v").T
-    if cfg["qkv_bias"]:
-        q = q + _w(lw, "b_q")
-        k = k + _w(lw, "b_k")
-        v = v + _w(lw, "b_v")
+    bias = cfg["qkv_bias"]
+    q = linear(h, _w(lw, "w_q"), _w(lw, "b_q") if bias else None)
+    k = linear(h, _w(lw, "w_k"), _w(lw, "b_k") if bias else None)
+    v = linear(h, _w(lw, "w_v"), _w(lw, "b_v") if bias else None)
     q, k, v = rb(q), rb(k), rb(v)
     q = q.reshape(B, Hq, D)
     k = k.reshape(B, Hkv, D)
@@ -164,6 +174,8 @@ def decode_layer(x, lw, cfg, k_cache, v_cache, positions, block_tables, round_bf
     for b in range(B):
         p = int(pos[b])
         blk = int(block_tables[b][p // bs])
+        if blk < 0:
+            raise ValueError(f"sequence {b}: no block allocated for position {p}")
         k_cache[blk, :, p % bs, :] = k[b]
         v_cache[blk, :, p % bs, :] = v[b]
 
@@ -171,12 +183,12 @@ def decode_layer(x, lw, cfg, k_cache, v_cache, positions, block_tables, round_bf
     for b in range(B):
         o[b] = paged_gqa_attention(q[b], k_cache, v_cache, block_tables[b], int(pos[b]) + 1, bs)
     o = rb(o.reshape(B, Hq * D))
-    x1 = x + o @ _w(lw, "w_o").T
+    x1 = x + linear(o, _w(lw, "w_o"))
 
     # FFN sub-block.
     h2 = rb(rms_norm(x1, _w(lw, "g_mlp"), cfg["rms_eps"]))
-    a = rb(silu(h2 @ _w(lw, "w_gate").T) * (h2 @ _w(lw, "w_up").T))
-    return x1 + a @ _w(lw, "w_down").T
+    a = rb(swiglu(h2, _w(lw, "w_gate"), _w(lw, "w_up")))
+    return x1 + linear(a, _w(lw, "w_down"))
 
 
 def decode_stack(x, layers, cfg, k_regions, v_regions, positions, block_tables, round_bf16=True):

@@ -1,0 +1,83 @@
+// Kernel launchers shared between the kernel sources and the host runtime.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sidp.h"
+
+namespace sidp {
+
+struct LinearCall {
+  const void* x;
+  int m, k;
+  const void* packed;
+  int n;
+  int epilogue;
+  const void* bias;
+  const float* residual;
+  void* out;
+  float* ws;
+  size_t ws_bytes;
+  int num_cus;
+};
+
+size_t packed_bytes(int n, int k);
+int gemm_splits(int M, int n_cols_packed, int K, int num_cus);
+size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus);
+hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s);
+hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, void* packed, hipStream_t s);
+hipError_t launch_linear(const LinearCall& c, hipStream_t s);
+
+hipError_t launch_rmsnorm(const float* x, const void* gain, float eps, void* out, int rows, int n, hipStream_t s);
+
+struct KvView {
+  uint16_t* k;            // [regions][nblk][Hkv][bs][D]
+  uint16_t* v;            // [regions][nblk][Hkv][D][bs]
+  int nblk, regions;
+  int hkv, d, bs;
+};
+
+struct RopeCall {
+  const uint16_t* qkv;
+  const int32_t* positions;
+  const int32_t* block_tables;
+  int max_blocks, batch;
+  int hq, hkv, d;
+  const uint16_t* g_q;
+  const uint16_t* g_k;
+  float qk_eps;
+  const float* rope_cos;  // [max_seq][D/2]
+  const float* rope_sin;
+  int max_seq;
+  KvView kv;
+  int region;
+  uint16_t* q_out;
+  uint32_t* err;
+};
+hipError_t launch_rope_append(const RopeCall& c, hipStream_t s);
+hipError_t launch_slot_mapping(const int32_t* positions, const int32_t* bt, int max_blocks, int batch, int bs,
+                               int nblk, int32_t* slots, uint32_t* err, hipStream_t s);
+
+struct AttnCall {
+  const uint16_t* q;  // [B][Hq][D]
+  const int32_t* positions;
+  const int32_t* block_tables;
+  int max_blocks, batch;
+  int hq, hkv, d;
+  KvView kv;
+  int region;
+  uint16_t* out;      // [B][Hq][D]
+  float* part;        // partials [B][Hq][max_parts][D + 2]
+  int max_parts;
+  uint32_t* err;
+};
+int attn_part_tokens();
+size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq);
+hipError_t launch_attention(const AttnCall& c, hipStream_t s);
+
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);
+hipError_t launch_poison(void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_spin(int64_t cycles, hipStream_t s);
+
+}  // namespace sidp

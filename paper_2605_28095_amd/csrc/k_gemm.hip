@@ -1,0 +1,352 @@
+// Dense projections of the decoder layer on gfx950 MFMA (bf16 in, fp32 accumulate):
+// QKV (+bias), O (+residual), gate/up (+SwiGLU), down (+residual).
+//
+// Shape of the problem: out[M, N] = X[M, K] * W[N, K]^T with M = decode batch
+// (8..512) and N, K in the thousands, so the weights dominate the bytes and
+// every weight byte must be read exactly once. Design:
+//  * Weights are packed once (into the layer's pool blob) in MFMA B-fragment
+//    order: for each group of 64 output columns, for each 16-wide k step,
+//    two 32x16 fragments of 64 lanes x 8 bf16. A wave that owns a column
+//    group streams its weights with 1 KB fully contiguous loads straight
+//    into registers; no LDS traffic for W.
+//  * Activations X are shared by the 4 waves of a workgroup: staged through
+//    LDS (64-wide k tiles, double buffered, 16-byte chunks XOR-swizzled by
+//    row so fragment reads spread over the banks).
+//  * A workgroup covers up to 256 rows x 256 columns; each wave holds
+//    MF x 2 accumulators of 32x32 (MF = rows / 32) and issues
+//    v_mfma_f32_32x32x16_bf16.
+//  * When the column tiles alone cannot fill the 256 CUs (N = 8192 gives 32
+//    tiles), K is split; each split writes fp32 partials and a reduction
+//    kernel sums them in split order (deterministic, so streamed and resident
+//    runs are bit-identical) and applies the epilogue.
+#include "common.h"
+#include "internal.h"
+
+namespace sidp {
+
+constexpr int kWaves = 4;          // waves per workgroup, one column group each
+constexpr int kBK = 64;            // k per LDS stage
+constexpr int kFragElems = 512;    // 64 lanes x 8 bf16
+
+__host__ __device__ inline int round_up(int a, int b) { return (a + b - 1) / b * b; }
+
+// ---------------------------------------------------------------- packing
+
+// W [N, K] -> packed [NP/64][KP/16][2][64][8], zero padded.
+__global__ void k_pack_linear(const uint16_t* __restrict__ w, int N, int K, int KB,
+                              int NG, uint16_t* __restrict__ out) {
+  const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // one 8-element chunk
+  const int64_t total = (int64_t)NG * KB * 2 * 64;
+  if (chunk >= total) return;
+  const int lane = (int)(chunk % 64);
+  const int nf = (int)((chunk / 64) % 2);
+  const int kb = (int)((chunk / 128) % KB);
+  const int ng = (int)(chunk / (128 * (int64_t)KB));
+  const int n = ng * 64 + nf * 32 + (lane % 32);
+  const int k0 = kb * 16 + (lane / 32) * 8;
+  uint16_t v[8];
+#pragma unroll
+  for (int i = 0; i < 8; i++) v[i] = (n < N && k0 + i < K) ? w[(int64_t)n * K + k0 + i] : (uint16_t)0;
+  uint16_t* dst = out + chunk * 8;
+#pragma unroll
+  for (int i = 0; i < 8; i++) dst[i] = v[i];
+}
+
+// gate, up [F, K] -> packed with n-group j = {gate rows 32j..32j+31, up rows 32j..32j+31}.
+__global__ void k_pack_gate_up(const uint16_t* __restrict__ wg, const uint16_t* __restrict__ wu, int F,
+                               int K, int KB, int NG, uint16_t* __restrict__ out) {
+  const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)NG * KB * 2 * 64;
+  if (chunk >= total) return;
+  const int lane = (int)(chunk % 64);
+  const int nf = (int)((chunk / 64) % 2);
+  const int kb = (int)((chunk / 128) % KB);
+  const int ng = (int)(chunk / (128 * (int64_t)KB));
+  const int f = ng * 32 + (lane % 32);
+  const int k0 = kb * 16 + (lane / 32) * 8;
+  const uint16_t* src = nf == 0 ? wg : wu;
+  uint16_t v[8];
+#pragma unroll
+  for (int i = 0; i < 8; i++) v[i] = (f < F && k0 + i < K) ? src[(int64_t)f * K + k0 + i] : (uint16_t)0;
+  uint16_t* dst = out + chunk * 8;
+#pragma unroll
+  for (int i = 0; i < 8; i++) dst[i] = v[i];
+}
+
+// ---------------------------------------------------------------- GEMM
+
+struct GemmArgs {
+  const uint16_t* x;   // [M, K] bf16, row stride K
+  const uint16_t* w;   // packed
+  int M, K, KP;        // KP = K rounded up to 64
+  int NG;              // packed column groups (64 columns each)
+  int tiles;           // ceil(NG / kWaves)
+  int splits;
+  int N;               // valid output columns (SWIGLU: F)
+  void* out;
+  const uint16_t* bias;  // EPI_BF16
+  const float* resid;    // EPI_RESID
+  float* ws;             // split-K partials [splits][M][NG*64]
+};
+
+__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+
+template <int MF>
+__device__ __forceinline__ void stage_x(const GemmArgs& a, int row0, int kt, u32x4_t (&xr)[MF]) {
+  const int k0 = kt * kBK;
+#pragma unroll
+  for (int i = 0; i < MF; i++) {
+    const int ci = threadIdx.x + i * 256;  // chunk index in [0, MF*32*8)
+    const int r = ci >> 3, cc = ci & 7;
+    const int row = row0 + r, k = k0 + cc * 8;
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    if (row < a.M && k < a.K) v = *(const u32x4_t*)(a.x + (int64_t)row * a.K + k);
+    xr[i] = v;
+  }
+}
+
+template <int MF>
+__device__ __forceinline__ void store_x(uint16_t* lds, const u32x4_t (&xr)[MF]) {
+#pragma unroll
+  for (int i = 0; i < MF; i++) {
+    const int ci = threadIdx.x + i * 256;
+    const int r = ci >> 3, cc = ci & 7;
+    *(u32x4_t*)(lds + r * kBK + ((cc ^ (r & 7)) << 3)) = xr[i];
+  }
+}
+
+__device__ __forceinline__ void load_w(const uint16_t* wg, int kt, int lane, u32x4_t (&wr)[8]) {
+  const uint16_t* p = wg + (int64_t)kt * 8 * kFragElems + lane * 8;
+#pragma unroll
+  for (int j = 0; j < 8; j++) wr[j] = *(const u32x4_t*)(p + j * kFragElems);
+}
+
+template <int MF, int EPI, bool PARTIAL>
+__global__ void __launch_bounds__(256) k_gemm(GemmArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  uint16_t* lds0 = smem;
+  uint16_t* lds1 = smem + MF * 32 * kBK;
+
+  const int split = blockIdx.x % a.splits;
+  const int tile = blockIdx.x / a.splits;
+  const int row0 = blockIdx.y * MF * 32;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int ng = tile * kWaves + wave;
+  const bool active = ng < a.NG;
+  const int KT = a.KP / kBK;
+  const int kt0 = (int)((int64_t)split * KT / a.splits);
+  const int kt1 = (int)((int64_t)(split + 1) * KT / a.splits);
+  const uint16_t* wg = a.w + (int64_t)(active ? ng : 0) * (a.KP / 16) * 2 * kFragElems;
+
+  f32x16_t acc[MF][2];
+#pragma unroll
+  for (int m = 0; m < MF; m++)
+#pragma unroll
+    for (int n = 0; n < 2; n++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) acc[m][n][r] = 0.f;
+
+  u32x4_t xr[MF];
+  u32x4_t wcur[8], wnxt[8];
+  if (kt0 < kt1) {
+    stage_x<MF>(a, row0, kt0, xr);
+    if (active) load_w(wg, kt0, lane, wcur);
+    store_x<MF>(lds0, xr);
+  }
+  __syncthreads();
+
+  for (int kt = kt0; kt < kt1; kt++) {
+    uint16_t* cur = ((kt - kt0) & 1) ? lds1 : lds0;
+    uint16_t* nxt = ((kt - kt0) & 1) ? lds0 : lds1;
+    const bool more = kt + 1 < kt1;
+    if (more) {
+      stage_x<MF>(a, row0, kt + 1, xr);
+      if (active) load_w(wg, kt + 1, lane, wnxt);
+    }
+    if (active) {
+#pragma unroll
+      for (int kb = 0; kb < 4; kb++) {
+        bf16x8_t af[MF];
+#pragma unroll
+        for (int m = 0; m < MF; m++) {
+          const int r = m * 32 + (lane & 31);
+          const int cc = kb * 2 + (lane >> 5);
+          af[m] = as_bf16x8(*(const u32x4_t*)(cur + r * kBK + ((cc ^ (r & 7)) << 3)));
+        }
+#pragma unroll
+        for (int m = 0; m < MF; m++) {
+          acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], as_bf16x8(wcur[kb * 2 + 0]), acc[m][0], 0, 0, 0);
+          acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], as_bf16x8(wcur[kb * 2 + 1]), acc[m][1], 0, 0, 0);
+        }
+      }
+    }
+    if (more) store_x<MF>(nxt, xr);
+    __syncthreads();
+    if (more) {
+#pragma unroll
+      for (int j = 0; j < 8; j++) wcur[j] = wnxt[j];
+    }
+  }
+
+  if (!active) return;
+  const int NP = a.NG * 64;
+#pragma unroll
+  for (int m = 0; m < MF; m++) {
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      const int row = row0 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      if (row >= a.M) continue;
+      if (PARTIAL) {
+        float* dst = a.ws + ((int64_t)split * a.M + row) * NP + ng * 64 + (lane & 31);
+        dst[0] = acc[m][0][r];
+        dst[32] = acc[m][1][r];
+      } else if (EPI == SIDP_EPI_SWIGLU) {
+        const int f = ng * 32 + (lane & 31);
+        if (f < a.N)
+          ((uint16_t*)a.out)[(int64_t)row * a.N + f] = f2bf(silu_f(acc[m][0][r]) * acc[m][1][r]);
+      } else {
+#pragma unroll
+        for (int nf = 0; nf < 2; nf++) {
+          const int n = ng * 64 + nf * 32 + (lane & 31);
+          if (n >= a.N) continue;
+          const int64_t o = (int64_t)row * a.N + n;
+          if (EPI == SIDP_EPI_BF16) {
+            float v = acc[m][nf][r];
+            if (a.bias) v += bf2f(a.bias[n]);
+            ((uint16_t*)a.out)[o] = f2bf(v);
+          } else {
+            ((float*)a.out)[o] = a.resid[o] + acc[m][nf][r];
+          }
+        }
+      }
+    }
+  }
+}
+
+// Sum split-K partials in split order and apply the epilogue.
+template <int EPI>
+__global__ void k_splitk_reduce(GemmArgs a) {
+  const int NP = a.NG * 64;
+  const int cols = EPI == SIDP_EPI_SWIGLU ? a.N : a.N;  // output columns
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)a.M * cols) return;
+  const int row = (int)(idx / cols), c = (int)(idx % cols);
+  if (EPI == SIDP_EPI_SWIGLU) {
+    const int pc = (c / 32) * 64 + (c % 32);
+    float g = 0.f, u = 0.f;
+    for (int s = 0; s < a.splits; s++) {
+      const float* p = a.ws + ((int64_t)s * a.M + row) * NP + pc;
+      g += p[0];
+      u += p[32];
+    }
+    ((uint16_t*)a.out)[idx] = f2bf(silu_f(g) * u);
+  } else {
+    const int pc = (c / 64) * 64 + (c % 64);  // packed column of output n (identity)
+    float v = 0.f;
+    for (int s = 0; s < a.splits; s++) v += a.ws[((int64_t)s * a.M + row) * NP + pc];
+    if (EPI == SIDP_EPI_BF16) {
+      if (a.bias) v += bf2f(a.bias[c]);
+      ((uint16_t*)a.out)[idx] = f2bf(v);
+    } else {
+      ((float*)a.out)[idx] = a.resid[idx] + v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- host side
+
+size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k, 64) * 2; }
+
+int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
+  const int NG = round_up(n_cols_packed, 64) / 64;
+  const int tiles = (NG + kWaves - 1) / kWaves;
+  const int mblocks = (M + 255) / 256;
+  const int KT = round_up(K, 64) / kBK;
+  const int base = tiles * mblocks;
+  int s = (num_cus + base / 2) / base;
+  if (s < 1) s = 1;
+  if (s > 8) s = 8;
+  if (s > KT) s = KT;
+  return s;
+}
+
+size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus) {
+  const int s = gemm_splits(M, n_cols_packed, K, num_cus);
+  if (s <= 1) return 0;
+  return (size_t)s * M * round_up(n_cols_packed, 64) * sizeof(float);
+}
+
+hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s) {
+  const int NG = round_up(n, 64) / 64, KB = round_up(k, 64) / 16;
+  const int64_t chunks = (int64_t)NG * KB * 128;
+  k_pack_linear<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>((const uint16_t*)w, n, k, KB, NG, (uint16_t*)packed);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, void* packed, hipStream_t s) {
+  const int F32 = round_up(f, 32);
+  const int NG = 2 * F32 / 64, KB = round_up(k, 64) / 16;
+  const int64_t chunks = (int64_t)NG * KB * 128;
+  k_pack_gate_up<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>((const uint16_t*)wg, (const uint16_t*)wu, f, k, KB,
+                                                                  NG, (uint16_t*)packed);
+  return hipGetLastError();
+}
+
+template <int MF, int EPI, bool P>
+static hipError_t launch_mf(const GemmArgs& a, int mblocks, hipStream_t s) {
+  const size_t lds = (size_t)2 * MF * 32 * kBK * sizeof(uint16_t);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm<MF, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  dim3 grid(a.tiles * a.splits, mblocks);
+  k_gemm<MF, EPI, P><<<grid, 256, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int EPI, bool P>
+static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  const int mblocks = (a.M + 255) / 256;
+  const int mrows = a.M <= 256 ? a.M : 256;
+  if (mrows <= 32) return launch_mf<1, EPI, P>(a, mblocks, s);
+  if (mrows <= 64) return launch_mf<2, EPI, P>(a, mblocks, s);
+  if (mrows <= 128) return launch_mf<4, EPI, P>(a, mblocks, s);
+  return launch_mf<8, EPI, P>(a, mblocks, s);
+}
+
+hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
+  GemmArgs a;
+  a.x = (const uint16_t*)c.x;
+  a.w = (const uint16_t*)c.packed;
+  a.M = c.m;
+  a.K = c.k;
+  a.KP = round_up(c.k, 64);
+  const int ncols = c.epilogue == SIDP_EPI_SWIGLU ? 2 * round_up(c.n, 32) : c.n;
+  a.NG = round_up(ncols, 64) / 64;
+  a.tiles = (a.NG + kWaves - 1) / kWaves;
+  a.splits = gemm_splits(c.m, ncols, c.k, c.num_cus);
+  a.N = c.n;
+  a.out = c.out;
+  a.bias = (const uint16_t*)c.bias;
+  a.resid = c.residual;
+  a.ws = c.ws;
+  if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
+  hipError_t e;
+  if (a.splits == 1) {
+    if (c.epilogue == SIDP_EPI_BF16) return launch_epi<SIDP_EPI_BF16, false>(a, s);
+    if (c.epilogue == SIDP_EPI_RESID) return launch_epi<SIDP_EPI_RESID, false>(a, s);
+    return launch_epi<SIDP_EPI_SWIGLU, false>(a, s);
+  }
+  e = launch_epi<SIDP_EPI_BF16, true>(a, s);  // partials only; epilogue in the reduction
+  if (e != hipSuccess) return e;
+  const int64_t outs = (int64_t)a.M * a.N;
+  const unsigned blocks = (unsigned)((outs + 255) / 256);
+  if (c.epilogue == SIDP_EPI_BF16) k_splitk_reduce<SIDP_EPI_BF16><<<blocks, 256, 0, s>>>(a);
+  else if (c.epilogue == SIDP_EPI_RESID) k_splitk_reduce<SIDP_EPI_RESID><<<blocks, 256, 0, s>>>(a);
+  else k_splitk_reduce<SIDP_EPI_SWIGLU><<<blocks, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace sidp

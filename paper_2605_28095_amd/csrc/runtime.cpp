@@ -1,0 +1,669 @@
+// Host runtime of the Weight-as-a-Service decode step: handle and config,
+// the layer blob layout of the weight pool, the two-slot cache ring driven by
+// HIP events, the paged-KV block allocator, and the per-layer kernel sequence.
+//
+// Paper: SiDP (arXiv 2605.28095). §4.2 "Asynchronous one-sided reading": the
+// non-owner issues non-blocking device-to-device copies of a layer's weights
+// into its local cache ahead of use (a lookahead window). §4.2 "Asynchronous
+// buffer management": pre-allocated slots; reserve a slot, issue reads,
+// attach a notification the compute waits on right before launch; the slot is
+// freed once compute signals done. §4.4: copies on separate streams,
+// notifications by events, no CPU barrier. Here the order is static (layers
+// are visited in order), so the housekeeper thread becomes two
+// hipStreamWaitEvent edges per layer and the ring needs no host thread.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/sidp.h"
+#include "internal.h"
+
+using namespace sidp;
+
+namespace {
+
+constexpr int kSlots = 2;
+constexpr size_t kAlign = 256;
+constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
+
+struct BlobLayout {
+  size_t g_attn, g_mlp, g_q, g_k, bias, w_qkv, w_o, w_gu, w_d, total;
+};
+
+int qkv_rows(const sidp_config& c) { return (c.num_q_heads + 2 * c.num_kv_heads) * c.head_dim; }
+
+BlobLayout blob_layout(const sidp_config& c) {
+  BlobLayout b;
+  size_t o = 0;
+  const size_t H = (size_t)c.hidden, D = (size_t)c.head_dim;
+  b.g_attn = o; o = align_up(o + H * 2, kAlign);
+  b.g_mlp = o;  o = align_up(o + H * 2, kAlign);
+  b.g_q = o;    o = align_up(o + (c.qk_norm ? D * 2 : 0), kAlign);
+  b.g_k = o;    o = align_up(o + (c.qk_norm ? D * 2 : 0), kAlign);
+  b.bias = o;   o = align_up(o + (c.qkv_bias ? (size_t)qkv_rows(c) * 2 : 0), kAlign);
+  b.w_qkv = o;  o = align_up(o + packed_bytes(qkv_rows(c), c.hidden), kAlign);
+  b.w_o = o;    o = align_up(o + packed_bytes(c.hidden, c.num_q_heads * c.head_dim), kAlign);
+  b.w_gu = o;   o = align_up(o + packed_bytes(2 * round_up_i(c.ffn_dim, 32), c.hidden), kAlign);
+  b.w_d = o;    o = align_up(o + packed_bytes(c.hidden, c.ffn_dim), kAlign);
+  b.total = o;
+  return b;
+}
+
+bool config_ok(const sidp_config* c) {
+  if (!c) return false;
+  if (c->num_layers < 1 || c->hidden < 64 || c->hidden % 64) return false;
+  if (c->head_dim != 64 && c->head_dim != 128) return false;
+  if (c->num_q_heads < 1 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads) return false;
+  if (c->num_q_heads / c->num_kv_heads > 16) return false;
+  if (c->ffn_dim < 16 || c->ffn_dim % 16) return false;
+  if (c->block_size != 16) return false;
+  if (c->max_batch < 1 || c->max_batch > 4096) return false;
+  if (c->max_seq_len < 1 || c->max_seq_len > (1 << 20)) return false;
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return false;
+  if (c->qk_norm && !(c->qk_norm_eps > 0.f)) return false;
+  return true;
+}
+
+// Ring operation kinds (shared with sidp_plan).
+enum { OP_FILL = 0, OP_WAIT_FILL = 1, OP_COMPUTE = 2, OP_DONE = 3, OP_WAIT_DONE = 4 };
+struct RingOp {
+  int kind;
+  int64_t g;
+  int slot;
+};
+
+// The static ring plan. Before the first streamed layer: fills of the first
+// kSlots layers. For layer g: compute side {wait fill g, compute g, done g};
+// copy side {wait done g, fill g + kSlots} into the slot g just released.
+void ring_prologue(int64_t g0, std::vector<RingOp>& copy_ops) {
+  for (int i = 0; i < kSlots; i++) copy_ops.push_back({OP_FILL, g0 + i, (int)((g0 + i) % kSlots)});
+}
+void ring_layer(int64_t g, std::vector<RingOp>& copy_ops, std::vector<RingOp>& compute_ops) {
+  const int s = (int)(g % kSlots);
+  compute_ops.push_back({OP_WAIT_FILL, g, s});
+  compute_ops.push_back({OP_COMPUTE, g, s});
+  compute_ops.push_back({OP_DONE, g, s});
+  copy_ops.push_back({OP_WAIT_DONE, g, s});
+  copy_ops.push_back({OP_FILL, g + kSlots, s});
+}
+
+}  // namespace
+
+struct sidp_handle {
+  sidp_config cfg;
+  BlobLayout blob;
+  int device = 0, num_cus = 256;
+  int last_hip = 0;
+  bool poisoned = false;
+  // pool and slots (caller-owned)
+  uint8_t* pool = nullptr;
+  size_t pool_bytes = 0;
+  uint8_t* slots = nullptr;
+  size_t slots_bytes = 0;
+  std::vector<char> loaded;
+  // KV caches (caller-owned)
+  uint16_t* k_cache = nullptr;
+  uint16_t* v_cache = nullptr;
+  int nblk = 0, regions = 0;
+  // library-owned device memory
+  uint16_t *h = nullptr, *qkv = nullptr, *q = nullptr, *o = nullptr, *act = nullptr;
+  float* ws = nullptr;
+  size_t ws_bytes = 0;
+  float* attn_part = nullptr;
+  int attn_max_parts = 0;
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  uint32_t* err = nullptr;
+  hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {};
+  bool events_ok = false;
+  // ring state
+  bool ring_started = false;
+  int64_t ring_g = 0;  // global index of the next streamed layer
+  int copy_grid = 512;
+  hipStream_t last_compute = nullptr, last_copy = nullptr;
+  bool any_copy = false;
+};
+
+#define HIPCHK(h, expr)                \
+  do {                                 \
+    hipError_t e_ = (expr);            \
+    if (e_ != hipSuccess) {            \
+      (h)->last_hip = (int)e_;         \
+      (h)->poisoned = true;            \
+      return SIDP_EHIP;                \
+    }                                  \
+  } while (0)
+
+extern "C" {
+
+const char* sidp_strerror(int code) {
+  switch (code) {
+    case SIDP_OK: return "ok";
+    case SIDP_EINVAL: return "invalid argument or device-side input error";
+    case SIDP_ENOBLOCKS: return "paged-KV blocks or block-table width exhausted";
+    case SIDP_ESTATE: return "call out of order or handle poisoned";
+    case SIDP_EHIP: return "HIP runtime error";
+    case SIDP_ENOMEM: return "device memory allocation failed";
+    default: return "unknown status";
+  }
+}
+
+int sidp_last_hip_error(const sidp_handle* h) { return h ? h->last_hip : 0; }
+
+size_t sidp_layer_bytes(const sidp_config* cfg) {
+  if (!config_ok(cfg)) return 0;
+  return blob_layout(*cfg).total;
+}
+
+static void free_device(sidp_handle* h) {
+  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->rope_cos, h->rope_sin, h->err};
+  for (void* p : ptrs)
+    if (p) (void)hipFree(p);
+  for (int i = 0; i < kSlots; i++) {
+    if (h->filled[i]) (void)hipEventDestroy(h->filled[i]);
+    if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
+  }
+}
+
+int sidp_create(const sidp_config* cfg, sidp_handle** out) {
+  if (!out) return SIDP_EINVAL;
+  *out = nullptr;
+  if (!config_ok(cfg)) return SIDP_EINVAL;
+  sidp_handle* h = new (std::nothrow) sidp_handle();
+  if (!h) return SIDP_ENOMEM;
+  h->cfg = *cfg;
+  h->blob = blob_layout(*cfg);
+  h->loaded.assign(cfg->num_layers, 0);
+  const sidp_config& c = *cfg;
+  auto fail = [&](int code) {
+    free_device(h);
+    delete h;
+    return code;
+  };
+  if (hipGetDevice(&h->device) != hipSuccess) return fail(SIDP_EHIP);
+  if (hipDeviceGetAttribute(&h->num_cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess)
+    return fail(SIDP_EHIP);
+  if (const char* g = std::getenv("SIDP_COPY_GRID")) h->copy_grid = std::max(1, std::atoi(g));
+
+  const size_t B = (size_t)c.max_batch, H = (size_t)c.hidden, D = (size_t)c.head_dim;
+  const size_t QD = (size_t)c.num_q_heads * D;
+  size_t ws = 0;
+  for (int m = 1; m <= c.max_batch; m++) {
+    ws = std::max(ws, gemm_ws_bytes(m, qkv_rows(c), c.hidden, h->num_cus));
+    ws = std::max(ws, gemm_ws_bytes(m, c.hidden, (int)QD, h->num_cus));
+    ws = std::max(ws, gemm_ws_bytes(m, 2 * round_up_i(c.ffn_dim, 32), c.hidden, h->num_cus));
+    ws = std::max(ws, gemm_ws_bytes(m, c.hidden, c.ffn_dim, h->num_cus));
+  }
+  h->ws_bytes = ws;
+  const int max_seq16 = round_up_i(c.max_seq_len, 16);
+  h->attn_max_parts = (max_seq16 + attn_part_tokens() - 1) / attn_part_tokens();
+  const size_t part_bytes = attn_ws_bytes(c.max_batch, c.num_q_heads, c.head_dim, max_seq16);
+  struct {
+    void** p;
+    size_t bytes;
+  } allocs[] = {
+      {(void**)&h->h, B * H * 2},
+      {(void**)&h->qkv, B * (size_t)qkv_rows(c) * 2},
+      {(void**)&h->q, B * QD * 2},
+      {(void**)&h->o, B * QD * 2},
+      {(void**)&h->act, B * (size_t)c.ffn_dim * 2},
+      {(void**)&h->ws, std::max<size_t>(ws, 256)},
+      {(void**)&h->attn_part, std::max<size_t>(part_bytes, 256)},
+      {(void**)&h->rope_cos, (size_t)c.max_seq_len * (D / 2) * 4},
+      {(void**)&h->rope_sin, (size_t)c.max_seq_len * (D / 2) * 4},
+      {(void**)&h->err, 256},
+  };
+  for (auto& a : allocs)
+    if (hipMalloc(a.p, a.bytes) != hipSuccess) return fail(SIDP_ENOMEM);
+  if (hipMemset(h->err, 0, 256) != hipSuccess) return fail(SIDP_EHIP);
+
+  // RoPE table: angle p * theta^(-2i/D) in double, stored as fp32 cos/sin.
+  std::vector<float> cs((size_t)c.max_seq_len * (D / 2)), sn(cs.size());
+  for (int p = 0; p < c.max_seq_len; p++)
+    for (size_t i = 0; i < D / 2; i++) {
+      const double ang = (double)p * std::pow((double)c.rope_theta, -2.0 * (double)i / (double)D);
+      cs[(size_t)p * (D / 2) + i] = (float)std::cos(ang);
+      sn[(size_t)p * (D / 2) + i] = (float)std::sin(ang);
+    }
+  if (hipMemcpy(h->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess) return fail(SIDP_EHIP);
+  if (hipMemcpy(h->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) return fail(SIDP_EHIP);
+  for (int i = 0; i < kSlots; i++) {
+    if (hipEventCreateWithFlags(&h->filled[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
+    if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
+  }
+  *out = h;
+  return SIDP_OK;
+}
+
+int sidp_destroy(sidp_handle* h) {
+  if (!h) return SIDP_EINVAL;
+  (void)hipDeviceSynchronize();
+  free_device(h);
+  delete h;
+  return SIDP_OK;
+}
+
+int sidp_pool_init(sidp_handle* h, void* pool, size_t pool_bytes, void* slots, size_t slots_bytes) {
+  if (!h) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  const size_t lb = h->blob.total;
+  if (!pool || pool_bytes < lb * (size_t)h->cfg.num_layers || ((uintptr_t)pool % kAlign)) return SIDP_EINVAL;
+  if (slots && (slots_bytes < lb * kSlots || ((uintptr_t)slots % kAlign))) return SIDP_EINVAL;
+  h->pool = (uint8_t*)pool;
+  h->pool_bytes = pool_bytes;
+  h->slots = (uint8_t*)slots;
+  h->slots_bytes = slots ? slots_bytes : 0;
+  h->loaded.assign(h->cfg.num_layers, 0);
+  h->ring_started = false;
+  h->ring_g = 0;
+  return SIDP_OK;
+}
+
+int sidp_pool_load_layer(sidp_handle* h, int32_t layer, const sidp_layer_weights* w, void* stream) {
+  if (!h || !w) return SIDP_EINVAL;
+  if (h->poisoned || !h->pool) return SIDP_ESTATE;
+  const sidp_config& c = h->cfg;
+  if (layer < 0 || layer >= c.num_layers) return SIDP_EINVAL;
+  if (!w->w_q || !w->w_k || !w->w_v || !w->w_o || !w->w_gate || !w->w_up || !w->w_down || !w->g_attn || !w->g_mlp)
+    return SIDP_EINVAL;
+  if (c.qkv_bias && (!w->b_q || !w->b_k || !w->b_v)) return SIDP_EINVAL;
+  if (c.qk_norm && (!w->g_q || !w->g_k)) return SIDP_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* base = h->pool + (size_t)layer * h->blob.total;
+  const size_t H = c.hidden, D = c.head_dim, QD = (size_t)c.num_q_heads * D, KD = (size_t)c.num_kv_heads * D;
+  HIPCHK(h, hipMemcpyAsync(base + h->blob.g_attn, w->g_attn, H * 2, hipMemcpyDeviceToDevice, s));
+  HIPCHK(h, hipMemcpyAsync(base + h->blob.g_mlp, w->g_mlp, H * 2, hipMemcpyDeviceToDevice, s));
+  if (c.qk_norm) {
+    HIPCHK(h, hipMemcpyAsync(base + h->blob.g_q, w->g_q, D * 2, hipMemcpyDeviceToDevice, s));
+    HIPCHK(h, hipMemcpyAsync(base + h->blob.g_k, w->g_k, D * 2, hipMemcpyDeviceToDevice, s));
+  }
+  if (c.qkv_bias) {
+    HIPCHK(h, hipMemcpyAsync(base + h->blob.bias, w->b_q, QD * 2, hipMemcpyDeviceToDevice, s));
+    HIPCHK(h, hipMemcpyAsync(base + h->blob.bias + QD * 2, w->b_k, KD * 2, hipMemcpyDeviceToDevice, s));
+    HIPCHK(h, hipMemcpyAsync(base + h->blob.bias + (QD + KD) * 2, w->b_v, KD * 2, hipMemcpyDeviceToDevice, s));
+  }
+  // Fused QKV: the q, k and v row blocks are multiples of 64 rows, so their
+  // packed forms concatenate along the column groups.
+  uint8_t* wqkv = base + h->blob.w_qkv;
+  HIPCHK(h, launch_pack_linear(w->w_q, (int)QD, (int)H, wqkv, s));
+  HIPCHK(h, launch_pack_linear(w->w_k, (int)KD, (int)H, wqkv + packed_bytes((int)QD, (int)H), s));
+  HIPCHK(h, launch_pack_linear(w->w_v, (int)KD, (int)H, wqkv + packed_bytes((int)(QD + KD), (int)H), s));
+  HIPCHK(h, launch_pack_linear(w->w_o, (int)H, (int)QD, base + h->blob.w_o, s));
+  HIPCHK(h, launch_pack_gate_up(w->w_gate, w->w_up, c.ffn_dim, (int)H, base + h->blob.w_gu, s));
+  HIPCHK(h, launch_pack_linear(w->w_down, (int)H, c.ffn_dim, base + h->blob.w_d, s));
+  h->loaded[layer] = 1;
+  return SIDP_OK;
+}
+
+// ---------------------------------------------------------------- paged KV
+
+static uint64_t splitmix64_next(uint64_t* state) {
+  uint64_t z = (*state += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+int sidp_kv_alloc(int32_t batch, const int32_t* ctx_lens, int32_t reserve_tokens, int32_t block_size,
+                  int32_t num_phys_blocks, uint64_t seed, int32_t max_blocks_per_seq, int32_t* block_tables) {
+  if (batch < 0 || reserve_tokens < 0 || block_size < 1 || num_phys_blocks < 0 || max_blocks_per_seq < 1)
+    return SIDP_EINVAL;
+  if (batch > 0 && (!ctx_lens || !block_tables)) return SIDP_EINVAL;
+  std::vector<int32_t> perm((size_t)num_phys_blocks);
+  for (int32_t i = 0; i < num_phys_blocks; i++) perm[i] = i;
+  uint64_t st = seed;
+  for (int32_t i = num_phys_blocks - 1; i >= 1; i--) {
+    const uint64_t j = splitmix64_next(&st) % (uint64_t)(i + 1);
+    std::swap(perm[i], perm[j]);
+  }
+  int64_t next = 0;
+  for (int32_t b = 0; b < batch; b++) {
+    if (ctx_lens[b] < 0) return SIDP_EINVAL;
+    const int64_t need = ((int64_t)ctx_lens[b] + reserve_tokens + block_size - 1) / block_size;
+    if (need > max_blocks_per_seq || next + need > num_phys_blocks) return SIDP_ENOBLOCKS;
+    int32_t* row = block_tables + (int64_t)b * max_blocks_per_seq;
+    for (int64_t j = 0; j < max_blocks_per_seq; j++) row[j] = j < need ? perm[next + j] : -1;
+    next += need;
+  }
+  return SIDP_OK;
+}
+
+size_t sidp_kv_region_bytes(const sidp_config* cfg, int32_t num_phys_blocks) {
+  if (!config_ok(cfg) || num_phys_blocks < 1) return 0;
+  return (size_t)num_phys_blocks * cfg->num_kv_heads * cfg->block_size * cfg->head_dim * 2;
+}
+
+int sidp_kv_attach(sidp_handle* h, void* k_cache, void* v_cache, int32_t num_phys_blocks, int32_t num_regions) {
+  if (!h || !k_cache || !v_cache || num_phys_blocks < 1 || num_regions < 1) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  if (((uintptr_t)k_cache % 16) || ((uintptr_t)v_cache % 16)) return SIDP_EINVAL;
+  h->k_cache = (uint16_t*)k_cache;
+  h->v_cache = (uint16_t*)v_cache;
+  h->nblk = num_phys_blocks;
+  h->regions = num_regions;
+  return SIDP_OK;
+}
+
+// ---------------------------------------------------------------- decode step
+
+static KvView kv_view(const sidp_handle* h) {
+  KvView v;
+  v.k = h->k_cache;
+  v.v = h->v_cache;
+  v.nblk = h->nblk;
+  v.regions = h->regions;
+  v.hkv = h->cfg.num_kv_heads;
+  v.d = h->cfg.head_dim;
+  v.bs = h->cfg.block_size;
+  return v;
+}
+
+static LinearCall linear_call(const sidp_handle* h, const void* x, int m, int k, const void* packed, int n, int epi,
+                              const void* bias, const float* resid, void* out) {
+  LinearCall c;
+  c.x = x;
+  c.m = m;
+  c.k = k;
+  c.packed = packed;
+  c.n = n;
+  c.epilogue = epi;
+  c.bias = bias;
+  c.residual = resid;
+  c.out = out;
+  c.ws = h->ws;
+  c.ws_bytes = h->ws_bytes;
+  c.num_cus = h->num_cus;
+  return c;
+}
+
+// The per-layer kernel sequence, reading weights from `wb` (a pool blob or a slot).
+static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, const int32_t* positions,
+                            const int32_t* bt, int max_blocks, int B, hipStream_t s) {
+  const sidp_config& c = h->cfg;
+  const BlobLayout& L = h->blob;
+  const int H = c.hidden, D = c.head_dim, QD = c.num_q_heads * D;
+  hipError_t e;
+  // a2: RMSNorm before attention
+  if ((e = launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s)) != hipSuccess) return e;
+  // a3: QKV projection (+ bias)
+  if ((e = launch_linear(linear_call(h, h->h, B, H, wb + L.w_qkv, qkv_rows(c), SIDP_EPI_BF16,
+                                     c.qkv_bias ? wb + L.bias : nullptr, nullptr, h->qkv), s)) != hipSuccess)
+    return e;
+  // a4/a5: QK-norm, RoPE, KV append at the slot of each sequence's position
+  RopeCall r;
+  r.qkv = h->qkv;
+  r.positions = positions;
+  r.block_tables = bt;
+  r.max_blocks = max_blocks;
+  r.batch = B;
+  r.hq = c.num_q_heads;
+  r.hkv = c.num_kv_heads;
+  r.d = D;
+  r.g_q = c.qk_norm ? (const uint16_t*)(wb + L.g_q) : nullptr;
+  r.g_k = c.qk_norm ? (const uint16_t*)(wb + L.g_k) : nullptr;
+  r.qk_eps = c.qk_norm_eps;
+  r.rope_cos = h->rope_cos;
+  r.rope_sin = h->rope_sin;
+  r.max_seq = c.max_seq_len;
+  r.kv = kv_view(h);
+  r.region = layer % h->regions;
+  r.q_out = h->q;
+  r.err = h->err;
+  if ((e = launch_rope_append(r, s)) != hipSuccess) return e;
+  // a6: paged GQA attention
+  AttnCall a;
+  a.q = h->q;
+  a.positions = positions;
+  a.block_tables = bt;
+  a.max_blocks = max_blocks;
+  a.batch = B;
+  a.hq = c.num_q_heads;
+  a.hkv = c.num_kv_heads;
+  a.d = D;
+  a.kv = kv_view(h);
+  a.region = layer % h->regions;
+  a.out = h->o;
+  a.part = h->attn_part;
+  a.max_parts = h->attn_max_parts;
+  a.err = h->err;
+  if ((e = launch_attention(a, s)) != hipSuccess) return e;
+  // a7: O projection + residual (in place on the fp32 residual stream)
+  if ((e = launch_linear(linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s)) !=
+      hipSuccess)
+    return e;
+  // a8: RMSNorm before the FFN
+  if ((e = launch_rmsnorm(hidden, wb + L.g_mlp, c.rms_eps, h->h, B, H, s)) != hipSuccess) return e;
+  // a9: gate/up projection + SwiGLU
+  if ((e = launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
+                         s)) != hipSuccess)
+    return e;
+  // a10: down projection + residual
+  return launch_linear(linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s);
+}
+
+// One slot fill on the copy stream: layer (g mod L) from the pool into `slot`.
+static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, int flags, hipStream_t cp) {
+  const size_t lb = h->blob.total;
+  uint8_t* dst = h->slots + (size_t)slot * lb;
+  const uint8_t* src = h->pool + (size_t)(g % h->cfg.num_layers) * lb;
+  hipError_t e;
+  if (flags & SIDP_DEBUG_POISON)
+    if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
+  if (flags & SIDP_DEBUG_DELAY)
+    if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
+  if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst, src, lb, hipMemcpyDeviceToDevice, cp);
+  else e = launch_copy(src, dst, lb, h->copy_grid, cp);
+  if (e != hipSuccess) return e;
+  return hipEventRecord(h->filled[slot], cp);
+}
+
+int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, const int32_t* block_tables,
+                     int32_t max_blocks_per_seq, int32_t batch, int32_t flags, void* compute, void* copy) {
+  if (!h) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  const sidp_config& c = h->cfg;
+  if (!hidden || !positions || !block_tables || batch < 1 || batch > c.max_batch || max_blocks_per_seq < 1)
+    return SIDP_EINVAL;
+  if (!h->pool || !h->k_cache) return SIDP_ESTATE;
+  for (int l = 0; l < c.num_layers; l++)
+    if (!h->loaded[l]) return SIDP_ESTATE;
+  const int parts = (max_blocks_per_seq * c.block_size + attn_part_tokens() - 1) / attn_part_tokens();
+  if (parts > h->attn_max_parts) return SIDP_EINVAL;
+  const bool streamed = flags & SIDP_STREAMED;
+  hipStream_t cs = (hipStream_t)compute, cp = (hipStream_t)copy;
+  if (streamed && (!h->slots || cp == cs)) return SIDP_EINVAL;
+  h->last_compute = cs;
+
+  if (!streamed) {
+    for (int l = 0; l < c.num_layers; l++)
+      HIPCHK(h, run_layer(h, h->pool + (size_t)l * h->blob.total, l, hidden, positions, block_tables,
+                          max_blocks_per_seq, batch, cs));
+    return SIDP_OK;
+  }
+
+  h->last_copy = cp;
+  h->any_copy = true;
+  std::vector<RingOp> copy_ops, compute_ops;
+  if (!h->ring_started) {
+    ring_prologue(h->ring_g, copy_ops);
+    h->ring_started = true;
+  }
+  for (RingOp& op : copy_ops) HIPCHK(h, issue_fill(h, op.g, op.slot, flags, cp));
+  copy_ops.clear();
+  for (int l = 0; l < c.num_layers; l++) {
+    const int64_t g = h->ring_g++;
+    ring_layer(g, copy_ops, compute_ops);
+    for (RingOp& op : compute_ops) {
+      if (op.kind == OP_WAIT_FILL) HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
+      else if (op.kind == OP_COMPUTE)
+        HIPCHK(h, run_layer(h, h->slots + (size_t)op.slot * h->blob.total, (int)(op.g % c.num_layers), hidden,
+                            positions, block_tables, max_blocks_per_seq, batch, cs));
+      else if (op.kind == OP_DONE) HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
+    }
+    for (RingOp& op : copy_ops) {
+      if (op.kind == OP_WAIT_DONE) HIPCHK(h, hipStreamWaitEvent(cp, h->consumed[op.slot], 0));
+      else if (op.kind == OP_FILL) HIPCHK(h, issue_fill(h, op.g, op.slot, flags, cp));
+    }
+    copy_ops.clear();
+    compute_ops.clear();
+  }
+  return SIDP_OK;
+}
+
+int sidp_sync(sidp_handle* h) {
+  if (!h) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  HIPCHK(h, hipStreamSynchronize(h->last_compute));
+  if (h->any_copy) HIPCHK(h, hipStreamSynchronize(h->last_copy));
+  HIPCHK(h, hipDeviceSynchronize());
+  uint32_t err = 0;
+  HIPCHK(h, hipMemcpy(&err, h->err, 4, hipMemcpyDeviceToHost));
+  if (err) {
+    HIPCHK(h, hipMemset(h->err, 0, 4));
+    return SIDP_EINVAL;
+  }
+  return SIDP_OK;
+}
+
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t* copy_ops, int32_t* n_copy, int32_t* compute_ops,
+              int32_t* n_compute) {
+  if (num_layers < 1 || steps < 0 || !n_copy || !n_compute) return SIDP_EINVAL;
+  std::vector<RingOp> cp, co;
+  if (steps > 0) ring_prologue(0, cp);
+  for (int64_t g = 0; g < (int64_t)num_layers * steps; g++) ring_layer(g, cp, co);
+  if ((int64_t)cp.size() > *n_copy || (int64_t)co.size() > *n_compute) return SIDP_EINVAL;
+  if ((!cp.empty() && !copy_ops) || (!co.empty() && !compute_ops)) return SIDP_EINVAL;
+  for (size_t i = 0; i < cp.size(); i++) {
+    copy_ops[3 * i] = cp[i].kind;
+    copy_ops[3 * i + 1] = (int32_t)cp[i].g;
+    copy_ops[3 * i + 2] = cp[i].slot;
+  }
+  for (size_t i = 0; i < co.size(); i++) {
+    compute_ops[3 * i] = co[i].kind;
+    compute_ops[3 * i + 1] = (int32_t)co[i].g;
+    compute_ops[3 * i + 2] = co[i].slot;
+  }
+  *n_copy = (int32_t)cp.size();
+  *n_compute = (int32_t)co.size();
+  return SIDP_OK;
+}
+
+// ---------------------------------------------------------------- single kernels
+
+int sidp_rmsnorm(const float* x, const void* gain, float eps, void* out, int32_t rows, int32_t n, void* stream) {
+  if (!x || !gain || !out || rows < 0 || n < 4 || n % 4 || !(eps > 0.f)) return SIDP_EINVAL;
+  return launch_rmsnorm(x, gain, eps, out, rows, n, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
+}
+
+size_t sidp_packed_bytes(int32_t n, int32_t k) {
+  if (n < 1 || k < 1) return 0;
+  return packed_bytes(n, k);
+}
+
+int sidp_pack_linear(const void* w, int32_t n, int32_t k, void* packed, void* stream) {
+  if (!w || !packed || n < 1 || k < 1) return SIDP_EINVAL;
+  return launch_pack_linear(w, n, k, packed, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
+}
+
+int sidp_pack_gate_up(const void* w_gate, const void* w_up, int32_t f, int32_t k, void* packed, void* stream) {
+  if (!w_gate || !w_up || !packed || f < 1 || k < 1) return SIDP_EINVAL;
+  return launch_pack_gate_up(w_gate, w_up, f, k, packed, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
+}
+
+int sidp_linear(sidp_handle* h, const void* x, int32_t m, int32_t k, const void* packed, int32_t n, int32_t epilogue,
+                const void* bias, const float* residual, void* out, void* stream) {
+  if (!h || !x || !packed || !out || m < 1 || m > h->cfg.max_batch || k < 8 || k % 8 || n < 1) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  if (epilogue < SIDP_EPI_BF16 || epilogue > SIDP_EPI_SWIGLU) return SIDP_EINVAL;
+  if (epilogue == SIDP_EPI_RESID && !residual) return SIDP_EINVAL;
+  if (epilogue != SIDP_EPI_BF16 && bias) return SIDP_EINVAL;
+  const int ncols = epilogue == SIDP_EPI_SWIGLU ? 2 * round_up_i(n, 32) : n;
+  if (gemm_ws_bytes(m, ncols, k, h->num_cus) > h->ws_bytes) return SIDP_EINVAL;
+  HIPCHK(h, launch_linear(linear_call(h, x, m, k, packed, n, epilogue, bias, residual, out), (hipStream_t)stream));
+  h->last_compute = (hipStream_t)stream;
+  return SIDP_OK;
+}
+
+int sidp_slot_mapping(sidp_handle* h, const int32_t* positions, const int32_t* block_tables,
+                      int32_t max_blocks_per_seq, int32_t batch, int32_t* slots, void* stream) {
+  if (!h || !positions || !block_tables || !slots || batch < 0 || max_blocks_per_seq < 1) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  const int nblk = h->nblk > 0 ? h->nblk : 0x7fffffff / h->cfg.block_size;
+  HIPCHK(h, launch_slot_mapping(positions, block_tables, max_blocks_per_seq, batch, h->cfg.block_size, nblk, slots,
+                                h->err, (hipStream_t)stream));
+  h->last_compute = (hipStream_t)stream;
+  return SIDP_OK;
+}
+
+int sidp_rope_append(sidp_handle* h, const void* qkv, const int32_t* positions, const int32_t* block_tables,
+                     int32_t max_blocks_per_seq, int32_t batch, const void* g_q, const void* g_k, int32_t region,
+                     void* q_out, void* stream) {
+  if (!h || !qkv || !positions || !block_tables || !q_out || batch < 0 || batch > h->cfg.max_batch) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  if (!h->k_cache || region < 0 || region >= h->regions || max_blocks_per_seq < 1) return SIDP_EINVAL;
+  if (h->cfg.qk_norm && (!g_q || !g_k)) return SIDP_EINVAL;
+  RopeCall r;
+  r.qkv = (const uint16_t*)qkv;
+  r.positions = positions;
+  r.block_tables = block_tables;
+  r.max_blocks = max_blocks_per_seq;
+  r.batch = batch;
+  r.hq = h->cfg.num_q_heads;
+  r.hkv = h->cfg.num_kv_heads;
+  r.d = h->cfg.head_dim;
+  r.g_q = h->cfg.qk_norm ? (const uint16_t*)g_q : nullptr;
+  r.g_k = h->cfg.qk_norm ? (const uint16_t*)g_k : nullptr;
+  r.qk_eps = h->cfg.qk_norm_eps;
+  r.rope_cos = h->rope_cos;
+  r.rope_sin = h->rope_sin;
+  r.max_seq = h->cfg.max_seq_len;
+  r.kv = kv_view(h);
+  r.region = region;
+  r.q_out = (uint16_t*)q_out;
+  r.err = h->err;
+  HIPCHK(h, launch_rope_append(r, (hipStream_t)stream));
+  h->last_compute = (hipStream_t)stream;
+  return SIDP_OK;
+}
+
+int sidp_attention(sidp_handle* h, const void* q, int32_t region, const int32_t* positions,
+                   const int32_t* block_tables, int32_t max_blocks_per_seq, int32_t batch, void* out, void* stream) {
+  if (!h || !q || !positions || !block_tables || !out || batch < 0 || batch > h->cfg.max_batch) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  if (!h->k_cache || region < 0 || region >= h->regions || max_blocks_per_seq < 1) return SIDP_EINVAL;
+  const int parts = (max_blocks_per_seq * h->cfg.block_size + attn_part_tokens() - 1) / attn_part_tokens();
+  if (parts > h->attn_max_parts) return SIDP_EINVAL;
+  AttnCall a;
+  a.q = (const uint16_t*)q;
+  a.positions = positions;
+  a.block_tables = block_tables;
+  a.max_blocks = max_blocks_per_seq;
+  a.batch = batch;
+  a.hq = h->cfg.num_q_heads;
+  a.hkv = h->cfg.num_kv_heads;
+  a.d = h->cfg.head_dim;
+  a.kv = kv_view(h);
+  a.region = region;
+  a.out = (uint16_t*)out;
+  a.part = h->attn_part;
+  a.max_parts = h->attn_max_parts;
+  a.err = h->err;
+  HIPCHK(h, launch_attention(a, (hipStream_t)stream));
+  h->last_compute = (hipStream_t)stream;
+  return SIDP_OK;
+}
+
+int sidp_copy(const void* src, void* dst, size_t bytes, int32_t grid, void* stream) {
+  if ((!src || !dst) && bytes) return SIDP_EINVAL;
+  if (((uintptr_t)src % 16) || ((uintptr_t)dst % 16) || grid < 0) return SIDP_EINVAL;
+  return launch_copy(src, dst, bytes, grid, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
+}
+
+}  // extern "C"

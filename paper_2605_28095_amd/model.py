@@ -1,0 +1,84 @@
+"""Device memory for one decoder stack, held in torch tensors, driven through
+the C ABI. torch provides allocations and streams only; all compute is in
+libsidp."""
+
+import torch
+
+from . import (
+    SIDP_STREAMED,
+    make_config,
+    sidp_create,
+    sidp_decode_step,
+    sidp_destroy,
+    sidp_kv_attach,
+    sidp_kv_region_bytes,
+    sidp_layer_bytes,
+    sidp_pool_init,
+    sidp_pool_load_layer,
+    sidp_sync,
+)
+
+
+class WaSDecoder:
+    """A weight pool of num_layers packed layer blobs, a 2-slot weight cache,
+    and num_regions paged KV regions of num_phys_blocks blocks each.
+
+    cfg: mapping with num_layers, hidden, num_q_heads, num_kv_heads, head_dim,
+    ffn_dim, qkv_bias, qk_norm, rms_eps, qk_norm_eps, rope_theta, block_size.
+    """
+
+    def __init__(self, cfg, max_batch, max_seq_len, num_phys_blocks, num_regions, device="cuda", slots=True):
+        self.cfg = dict(cfg)
+        self.device = torch.device(device)
+        self.config = make_config(cfg, max_batch, max_seq_len)
+        self.h = None
+        self.h = sidp_create(self.config)
+        self.layer_bytes = sidp_layer_bytes(self.config)
+        L = cfg["num_layers"]
+        self.pool = torch.empty(L * self.layer_bytes, dtype=torch.uint8, device=self.device)
+        self.slots = torch.empty(2 * self.layer_bytes, dtype=torch.uint8, device=self.device) if slots else None
+        for t in (self.pool, self.slots):
+            if t is not None and t.data_ptr() % 256:
+                raise RuntimeError("device allocation is not 256-byte aligned")
+        sidp_pool_init(self.h, self.pool, self.pool.numel(), self.slots,
+                       0 if self.slots is None else self.slots.numel())
+        self.num_phys_blocks = num_phys_blocks
+        self.num_regions = num_regions
+        region_elems = sidp_kv_region_bytes(self.config, num_phys_blocks) // 2
+        self.k_cache = torch.empty(num_regions * region_elems, dtype=torch.bfloat16, device=self.device)
+        self.v_cache = torch.empty(num_regions * region_elems, dtype=torch.bfloat16, device=self.device)
+        sidp_kv_attach(self.h, self.k_cache, self.v_cache, num_phys_blocks, num_regions)
+
+    # Cache views in the library's layouts.
+    def k_view(self):
+        c = self.cfg
+        return self.k_cache.view(self.num_regions, self.num_phys_blocks, c["num_kv_heads"], c["block_size"],
+                                 c["head_dim"])
+
+    def v_view(self):
+        """V blocks are stored transposed: [region][block][kv_head][d][token]."""
+        c = self.cfg
+        return self.v_cache.view(self.num_regions, self.num_phys_blocks, c["num_kv_heads"], c["head_dim"],
+                                 c["block_size"])
+
+    def load_layer(self, layer, weights, stream=None):
+        sidp_pool_load_layer(self.h, layer, weights, stream)
+
+    def step(self, hidden, positions, block_tables, flags=SIDP_STREAMED, compute=None, copy=None):
+        compute = compute if compute is not None else torch.cuda.current_stream(self.device)
+        sidp_decode_step(self.h, hidden, positions, block_tables, block_tables.shape[1], hidden.shape[0], flags,
+                         compute, copy)
+
+    def sync(self):
+        sidp_sync(self.h)
+
+    def close(self):
+        if self.h is not None:
+            sidp_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,102 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and its host-only logic (block-table allocation, slot-ring plan,
+argument validation) matches the oracle bit for bit. No GPU work is issued."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_symbols():
+    text = open(os.path.join(ROOT, "include", "sidp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sidp_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2605_28095_amd as sidp
+    syms = _header_symbols()
+    assert len(syms) >= 20
+    lib = ctypes.CDLL(sidp.LIB_PATH)
+    missing = [s for s in syms if not hasattr(lib, s)]
+    assert not missing, missing
+    assert sorted(sidp.EXPORTED) == syms
+
+
+def test_strerror_names_every_code():
+    import paper_2605_28095_amd as sidp
+    for code in (0, -1, -2, -3, -4, -5):
+        assert sidp.strerror(code) and sidp.strerror(code) != "unknown status"
+    assert sidp.strerror(7) == "unknown status"
+
+
+@pytest.mark.parametrize("name", ["tiny_layer", "qwen3_32b_layer", "llama70b_stack80"])
+def test_kv_alloc_bit_exact_vs_oracle(name):
+    import paper_2605_28095_amd as sidp
+    cfg = synth.get_config(name)
+    ctx = synth.context_lengths(cfg, seed=0)
+    reserve = 1
+    need = int(sum(-(-(int(c) + reserve) // 16) for c in ctx))
+    nblk = cfg["num_phys_blocks"] or need + 37
+    maxb = int(max(-(-(int(c) + reserve) // 16) for c in ctx)) + 2
+    for seed in (0, 1, 12345):
+        got = sidp.sidp_kv_alloc(ctx, reserve, 16, nblk, seed, maxb)
+        want = oracle.allocate_block_tables(ctx, reserve, nblk, maxb, seed)
+        assert got == want
+
+
+def test_kv_alloc_errors():
+    import paper_2605_28095_amd as sidp
+    with pytest.raises(sidp.SidpError) as e:
+        sidp.sidp_kv_alloc([100, 100], 1, 16, 10, 0, 16)
+    assert e.value.code == sidp.SIDP_ENOBLOCKS
+    with pytest.raises(sidp.SidpError) as e:
+        sidp.sidp_kv_alloc([100], 1, 16, 100, 0, 4)  # table too narrow
+    assert e.value.code == sidp.SIDP_ENOBLOCKS
+    with pytest.raises(sidp.SidpError) as e:
+        sidp.sidp_kv_alloc([-3], 1, 16, 100, 0, 4)
+    assert e.value.code == sidp.SIDP_EINVAL
+    assert sidp.sidp_kv_alloc([], 1, 16, 0, 0, 1) == []
+
+
+@pytest.mark.parametrize("L,steps", [(1, 1), (3, 2), (80, 3), (8, 0)])
+def test_plan_matches_oracle_schedule(L, steps):
+    import paper_2605_28095_amd as sidp
+    assert sidp.sidp_plan(L, steps) == tuple(list(x) for x in oracle.was_schedule(L, steps, 2))
+
+
+def test_config_validation_on_host():
+    import paper_2605_28095_amd as sidp
+    cfg = synth.get_config("llama70b_layer")
+    good = sidp.make_config(cfg, 256, 8192)
+    lb = sidp.sidp_layer_bytes(good)
+    # packed projections plus small vectors, all 256-byte aligned
+    assert lb % 256 == 0
+    assert 2 * synth.layer_param_count(cfg) <= lb < 2 * synth.layer_param_count(cfg) + 64 * 1024
+    for field, bad in [("head_dim", 96), ("num_kv_heads", 7), ("block_size", 32), ("hidden", 100),
+                       ("ffn_dim", 20), ("max_batch", 0)]:
+        c = sidp.make_config(cfg, 256, 8192)
+        setattr(c, field, bad)
+        assert sidp.sidp_layer_bytes(c) == 0, field
+    c = sidp.make_config(cfg, 256, 8192)
+    c.num_q_heads = 64
+    c.num_kv_heads = 2  # group of 32 query heads per KV head is not supported
+    assert sidp.sidp_layer_bytes(c) == 0
+    assert sidp.sidp_kv_region_bytes(good, 10) == 10 * 8 * 16 * 128 * 2
+    assert sidp.sidp_packed_bytes(688, 256) == 704 * 256 * 2
+
+
+def test_null_handle_calls_are_rejected():
+    import paper_2605_28095_amd as sidp
+    assert sidp.raw_call("sidp_sync", None) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_destroy", None) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_decode_step", None, None, None, None, 1, 1, 0, None, None) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_plan", 0, 1, None, None, None, None) == sidp.SIDP_EINVAL
