@@ -1,0 +1,285 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the Weight-as-a-Service path on one MI355X.
+
+Default workload: an 80-layer Llama-3.1-70B-shaped stack (hidden 8192, 64/8
+heads, head_dim 128, FFN 28672, bf16) at batch 256, context lengths uniform in
+[1024, 8192], 16-token paged KV. All 80 layers' weights (137 GB) sit in a pool
+region of HBM and stream through a 2-slot weight cache on a copy stream while
+the previous layer computes. The KV cache fills the HBM left over; layers share
+KV regions (layer l uses region l mod R) when there are fewer regions than
+layers. Inputs are seeded synthetic tensors already resident in HBM.
+
+Prints one JSON line: decode tokens/s (batch / step time), the roofline of the
+dominant kernel (live HIP-event timing inside the timed region), and the
+oracle's throughput on the host over a bounded sample.
+"""
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode tok/s at B=256 (70B-shape stack); MFMA util %; HBM GB/s"
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, published
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA, published
+
+DESCR = {
+    "llama70b_stack80": "Llama-3.1-70B-shaped 80-layer stack, weights streamed through a 2-slot HBM cache",
+    "qwen25_72b_stack8": "Qwen2.5-72B-shaped 8-layer stack, weights streamed through a 2-slot HBM cache",
+    "llama70b_layer": "Llama-3.1-70B-shaped single layer",
+    "qwen3_32b_layer": "Qwen3-32B-shaped single layer",
+    "tiny_layer": "tiny single layer",
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_work(cfg, B, seq_total, layer_bytes):
+    """Bytes and flops each kernel class must move / perform for one layer at
+    batch B (seq_total = sum over sequences of attended tokens)."""
+    H, D, F = cfg["hidden"], cfg["head_dim"], cfg["ffn_dim"]
+    Hq, Hkv = cfg["num_q_heads"], cfg["num_kv_heads"]
+    QD, KD = Hq * D, Hkv * D
+    NQKV = QD + 2 * KD
+    kv_tok = 2 * KD * 2  # K and V bytes per token
+    w = {
+        "norm_attn": (B * H * 4 + H * 2 + B * H * 2, 0),
+        "qkv": (NQKV * H * 2 + B * H * 2 + B * NQKV * 2, 2 * B * NQKV * H),
+        "rope_append": (B * NQKV * 2 + B * QD * 2 + B * kv_tok, 0),
+        "attention": (seq_total * kv_tok + 2 * B * QD * 2, 4 * Hq * D * seq_total),
+        "o_proj": (H * QD * 2 + B * QD * 2 + 2 * B * H * 4, 2 * B * H * QD),
+        "norm_mlp": (B * H * 4 + H * 2 + B * H * 2, 0),
+        "gate_up": (2 * F * H * 2 + B * H * 2 + B * F * 2, 2 * B * 2 * F * H),
+        "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4, 2 * B * H * F),
+        "fill": (2 * layer_bytes, 0),
+        "wait_fill": (0, 0),
+    }
+    return w
+
+
+def cpu_baseline(cfg, weights_for_layer, kv_rows, x_rows, pos_rows, tabs_rows, n_layers_sample):
+    """Times the oracle (as it stands) on a bounded sample: n_layers_sample
+    layers for the sampled rows; returns tokens/s extrapolated to the full
+    stack and the BLAS thread count it ran with."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    k_np, v_np = kv_rows
+    x = x_rows.copy()
+    t0 = time.perf_counter()
+    for l in range(n_layers_sample):
+        x = oracle.decode_layer(x, weights_for_layer(l), cfg, k_np.copy(), v_np.copy(), pos_rows, tabs_rows, True)
+    dt = time.perf_counter() - t0
+    rows = x.shape[0]
+    per_layer = dt / n_layers_sample
+    assert np.all(np.isfinite(x))
+    return rows / (per_layer * cfg["num_layers"]), threads, dt
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama70b_stack80")
+    ap.add_argument("--batch", type=int, default=256)
+    ap.add_argument("--mode", choices=["streamed", "resident"], default="streamed")
+    ap.add_argument("--copy", choices=["kernel", "memcpy"], default="kernel")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-resident-compare", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's share of the decode step; runs on more than one GPU are not "
+              "part of this build (see the sharding notes: each GPU would run this same step on its own "
+              "batch and pull non-owned layers over xGMI).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2605_28095_amd as sidp
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.get_config(args.workload)
+    B, L = args.batch, cfg["num_layers"]
+    ctx = synth.context_lengths(cfg, args.seed, B)
+    reserve = 1
+    need = [-(-(int(c) + reserve) // 16) for c in ctx]
+    nblk, maxb = int(sum(need)), int(max(need))
+    tables = sidp.sidp_kv_alloc(ctx, reserve, 16, nblk, args.seed, maxb)
+    max_seq = int(ctx.max()) + reserve + 16
+
+    config = sidp.make_config(cfg, B, max_seq)
+    layer_bytes = sidp.sidp_layer_bytes(config)
+    region_pair = 2 * sidp.sidp_kv_region_bytes(config, nblk)
+    free, total = torch.cuda.mem_get_info(dev)
+    margin = 24 << 30
+    if args.kv_regions > 0:
+        R = args.kv_regions
+    else:
+        R = int(min(L, (free - (L + 2) * layer_bytes - margin) // region_pair))
+    if R < 1:
+        raise SystemExit(f"not enough HBM: free {free / 1e9:.1f} GB, pool {L * layer_bytes / 1e9:.1f} GB")
+    log(f"{args.workload}: L={L} B={B} pool {L * layer_bytes / 1e9:.1f} GB, slots {2 * layer_bytes / 1e9:.2f} GB, "
+        f"KV {R} regions x {region_pair / 1e9:.2f} GB, free {free / 1e9:.1f} of {total / 1e9:.1f} GB")
+
+    t_setup = time.perf_counter()
+    dec = sidp.WaSDecoder(cfg, B, max_seq, nblk, R, device=dev, slots=(args.mode == "streamed"))
+    sample_rows = list(range(16))
+    sample_layers = min(8, L)
+    keep_w = {}
+    for l in range(L):
+        w = synth.layer_weights(cfg, l, seed=args.seed, device=dev)
+        dec.load_layer(l, w)
+        torch.cuda.synchronize()
+        if l < sample_layers and not args.no_cpu_baseline:
+            keep_w[l] = {k: v.view(torch.int16).cpu().numpy().view(np.uint16) for k, v in w.items()}
+        del w
+    log(f"pool loaded in {time.perf_counter() - t_setup:.1f}s")
+    k0, v0 = synth.kv_prefill(cfg, nblk, 0, seed=args.seed, device=dev)
+    # the oracle's sample: the sampled rows' blocks, straight from the generator
+    if not args.no_cpu_baseline:
+        import oracle
+        sel = np.concatenate([np.asarray(tables[r][:need[r]]) for r in sample_rows])
+        idx = torch.as_tensor(sel, dtype=torch.long, device=dev)
+        kv_rows = (oracle.bf16_bits_to_f64(k0.index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)),
+                   oracle.bf16_bits_to_f64(v0.index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)))
+        width = max(need[r] for r in sample_rows)
+        tabs_rows, o = [], 0
+        for r in sample_rows:
+            tabs_rows.append(list(range(o, o + need[r])) + [-1] * (width - need[r]))
+            o += need[r]
+    dec.k_view()[0].copy_(k0)
+    dec.v_view()[0].copy_(v0.transpose(-1, -2))
+    del k0, v0
+    for r in range(1, R):  # every region holds the same content; each layer still reads its own region
+        dec.k_view()[r].copy_(dec.k_view()[0])
+        dec.v_view()[r].copy_(dec.v_view()[0])
+    x0 = synth.hidden_input(cfg, args.seed, device=dev, batch=B)
+    hidden = x0.clone()
+    pos = torch.tensor(ctx, dtype=torch.int32, device=dev)
+    bt = torch.tensor(tables, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    log(f"setup done in {time.perf_counter() - t_setup:.1f}s")
+
+    compute = torch.cuda.current_stream(dev)
+    copy_stream = torch.cuda.Stream(dev) if args.mode == "streamed" else None
+    flags = sidp.SIDP_STREAMED if args.mode == "streamed" else sidp.SIDP_RESIDENT
+    if args.copy == "memcpy":
+        flags |= sidp.SIDP_COPY_MEMCPY
+
+    for i in range(args.warmup):
+        dec.step(hidden, pos, bt, flags, compute=compute, copy=copy_stream)
+    dec.sync()
+    sidp.sidp_timing_collect(dec.h)
+    log(f"warmup {args.warmup} steps done")
+
+    # timed region: exactly K steps, synchronized on both sides
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    e0.record(compute)
+    for i in range(args.steps):
+        dec.step(hidden, pos, bt, flags | sidp.SIDP_TIMING, compute=compute, copy=copy_stream)
+    e1.record(compute)
+    torch.cuda.synchronize()
+    dec.sync()
+    wall = time.perf_counter() - w0
+    ms_total = e0.elapsed_time(e1)
+    ms_per_step = ms_total / args.steps
+    value = B / (ms_per_step / 1e3)
+    timing = sidp.sidp_timing_collect(dec.h)
+    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step, {value:.1f} tok/s (wall {wall:.2f}s)")
+
+    seq_total = int(ctx.sum()) + B
+    work = algorithmic_work(cfg, B, seq_total, layer_bytes)
+    kernels = {}
+    for name, (ms, n) in timing.items():
+        if n == 0:
+            continue
+        avg = ms / n
+        byts, flops = work[name]
+        if avg <= 0 or byts == 0:
+            kernels[name] = {"launches": n, "ms_per_launch": round(avg, 5), "ms_per_step": round(ms / args.steps, 4)}
+            continue
+        kernels[name] = {
+            "launches": n, "ms_per_launch": round(avg, 5),
+            "ms_per_step": round(ms / args.steps, 4),
+            "GB_per_s": round(byts / (avg * 1e-3) / 1e9, 1),
+            "TFLOP_per_s": round(flops / (avg * 1e-3) / 1e12, 1) if flops else None,
+            "hbm_frac": round(byts / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "mfma_frac": round(flops / (avg * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4) if flops else None,
+            "bytes_per_launch": byts,
+        }
+    compute_classes = [k for k in kernels if k not in ("fill", "wait_fill")]
+    dom = max(compute_classes, key=lambda k: kernels[k]["ms_per_step"])
+    dk = kernels[dom]
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": dk["GB_per_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": dk["hbm_frac"], "traffic": None,
+                "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
+
+    resident_ms = None
+    if args.mode == "streamed" and not args.no_resident_compare:
+        for i in range(2):
+            dec.step(hidden, pos, bt, sidp.SIDP_RESIDENT, compute=compute)
+        torch.cuda.synchronize()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r0.record(compute)
+        nres = max(3, args.steps // 2)
+        for i in range(nres):
+            dec.step(hidden, pos, bt, sidp.SIDP_RESIDENT, compute=compute)
+        r1.record(compute)
+        torch.cuda.synchronize()
+        resident_ms = r0.elapsed_time(r1) / nres
+        log(f"resident (no streaming) {resident_ms:.2f} ms/step")
+    dec.sync()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        val, threads, dt = cpu_baseline(cfg, lambda l: keep_w[l], kv_rows, x0[sample_rows].double().cpu().numpy(),
+                                        ctx[sample_rows], np.asarray(tabs_rows), sample_layers)
+        cpu = {"value": round(val, 3), "unit": "tok/s", "cores": threads, "kind": "oracle",
+               "sample": f"{sample_layers} of {L} layers for {len(sample_rows)} of {B} sequences (full contexts), "
+                         f"float64 with bf16 storage rounding; {dt:.1f}s; tok/s = rows / (s per layer x {L})"}
+        log(f"oracle baseline: {val:.3f} tok/s over {dt:.1f}s with {threads} BLAS threads")
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {DESCR.get(args.workload, args.workload)}",
+            "global_batch": B, "layers": L, "seq_len": f"ctx U[{cfg['ctx_lo']},{cfg['ctx_hi']}], mean {ctx.mean():.0f}",
+            "parallelism": "single GPU", "mode": args.mode, "copy": args.copy, "kv_regions": R,
+            "layer_bytes": layer_bytes,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "resident_ms_per_step": round(resident_ms, 3) if resident_ms else None,
+        "fill_stall_ms_per_step": kernels["wait_fill"]["ms_per_step"] if "wait_fill" in kernels else None,
+    }
+    print(json.dumps(out), flush=True)
+    dec.close()
+
+
+if __name__ == "__main__":
+    main()

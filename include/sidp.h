@@ -56,6 +56,20 @@ extern "C" {
 #define SIDP_COPY_MEMCPY   0x2  /* slot fills by hipMemcpyAsync (default: library copy kernel) */
 #define SIDP_DEBUG_POISON  0x10 /* before each fill, write NaN bytes over the slot */
 #define SIDP_DEBUG_DELAY   0x20 /* before each fill, spin ~200 us on the copy stream */
+#define SIDP_TIMING        0x40 /* bracket each kernel class with HIP events (sidp_timing_collect) */
+
+/* ---- kernel classes timed under SIDP_TIMING ---- */
+#define SIDP_K_NORM_ATTN  0 /* RMSNorm before attention              */
+#define SIDP_K_QKV        1 /* QKV projection (+bias)                 */
+#define SIDP_K_ROPE       2 /* QK-norm + RoPE + KV append             */
+#define SIDP_K_ATTN       3 /* paged attention (+ partition combine)  */
+#define SIDP_K_O          4 /* O projection + residual                */
+#define SIDP_K_NORM_MLP   5 /* RMSNorm before the FFN                 */
+#define SIDP_K_GATE_UP    6 /* gate/up projection + SwiGLU            */
+#define SIDP_K_DOWN       7 /* down projection + residual             */
+#define SIDP_K_FILL       8 /* slot fill (copy stream)                */
+#define SIDP_K_WAIT_FILL  9 /* compute stream blocked on a slot fill  */
+#define SIDP_NUM_KCLASSES 10
 
 /* ---- sidp_linear epilogues ---- */
 #define SIDP_EPI_BF16    0 /* out bf16 [m, n] = x W^T (+ bias)                      */
@@ -175,6 +189,14 @@ int sidp_decode_step(sidp_handle *h, float *hidden, const int32_t *positions, co
  * SIDP_EINVAL if a kernel latched a device-side input error since the last
  * sync (and clears it), SIDP_EHIP on an asynchronous HIP error. */
 int sidp_sync(sidp_handle *h);
+
+/* ---- timing ----
+ * Waits for every event pair recorded under SIDP_TIMING since the last
+ * collect and returns, per kernel class, the summed elapsed milliseconds
+ * (ms[SIDP_NUM_KCLASSES], host) and the number of timed launches
+ * (launches[SIDP_NUM_KCLASSES], host); then recycles the events. Each pair
+ * brackets one layer's launches of that class on the stream they run on. */
+int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
 
 /* ---- the slot-ring plan (host only) ----
  * The order in which sidp_decode_step issues ring operations for `steps`

@@ -27,6 +27,10 @@ SIDP_STREAMED = 0x1
 SIDP_COPY_MEMCPY = 0x2
 SIDP_DEBUG_POISON = 0x10
 SIDP_DEBUG_DELAY = 0x20
+SIDP_TIMING = 0x40
+
+KERNEL_CLASSES = ["norm_attn", "qkv", "rope_append", "attention", "o_proj", "norm_mlp", "gate_up", "down", "fill",
+                  "wait_fill"]
 
 SIDP_EPI_BF16 = 0
 SIDP_EPI_RESID = 1
@@ -39,6 +43,7 @@ EXPORTED = [
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
+    "sidp_timing_collect",
 ]
 
 
@@ -97,6 +102,7 @@ _sigs = {
     "sidp_rope_append": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _P, _P, _I, _P, _P]),
     "sidp_attention": (ctypes.c_int, [_P, _P, _I, _P, _P, _I, _I, _P, _P]),
     "sidp_copy": (ctypes.c_int, [_P, _P, _Z, _I, _P]),
+    "sidp_timing_collect": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), _PI]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -248,6 +254,14 @@ def sidp_attention(h, q, region, positions, block_tables, max_blocks_per_seq, ba
 
 def sidp_copy(src, dst, nbytes, grid=0, stream=None):
     _check(_lib.sidp_copy(_ptr(src), _ptr(dst), nbytes, grid, _stream(stream)), "sidp_copy")
+
+
+def sidp_timing_collect(h):
+    """{kernel class: (total ms, launches)} for the SIDP_TIMING intervals since the last collect."""
+    ms = (ctypes.c_double * len(KERNEL_CLASSES))()
+    n = (ctypes.c_int32 * len(KERNEL_CLASSES))()
+    _check(_lib.sidp_timing_collect(h, ms, n), "sidp_timing_collect")
+    return {k: (ms[i], n[i]) for i, k in enumerate(KERNEL_CLASSES)}
 
 
 def raw_call(name, *args):

@@ -12,9 +12,11 @@
 //  * Activations X are shared by the 4 waves of a workgroup: staged through
 //    LDS (64-wide k tiles, double buffered, 16-byte chunks XOR-swizzled by
 //    row so fragment reads spread over the banks).
-//  * A workgroup covers up to 256 rows x 256 columns; each wave holds
-//    MF x 2 accumulators of 32x32 (MF = rows / 32) and issues
-//    v_mfma_f32_32x32x16_bf16.
+//  * A workgroup covers up to 256 rows x 256 columns with 4 or 8 waves; each
+//    wave holds MF x 2 accumulators of 32x32 (up to 128 rows x 64 columns)
+//    and issues v_mfma_f32_32x32x16_bf16; two waves share each SIMD.
+//  * Loads go through raw buffer resources: addresses stay in scalar
+//    registers, and an offset past the buffer reads zeros (row and K tails).
 //  * When the column tiles alone cannot fill the 256 CUs (N = 8192 gives 32
 //    tiles), K is split; each split writes fp32 partials and a reduction
 //    kernel sums them in split order (deterministic, so streamed and resident
@@ -91,52 +93,53 @@ struct GemmArgs {
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int MF>
-__device__ __forceinline__ void stage_x(const GemmArgs& a, int row0, int kt, u32x4_t (&xr)[MF]) {
-  const int k0 = kt * kBK;
-#pragma unroll
-  for (int i = 0; i < MF; i++) {
-    const int ci = threadIdx.x + i * 256;  // chunk index in [0, MF*32*8)
-    const int r = ci >> 3, cc = ci & 7;
-    const int row = row0 + r, k = k0 + cc * 8;
-    u32x4_t v = {0u, 0u, 0u, 0u};
-    if (row < a.M && k < a.K) v = *(const u32x4_t*)(a.x + (int64_t)row * a.K + k);
-    xr[i] = v;
-  }
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 raw buffer: 32-bit data, bounds-checked
+constexpr uint32_t kOutOfRange = 0x80000000u;  // any offset past num_records reads as zero
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, (int)kRsrcWord3);
 }
 
-template <int MF>
-__device__ __forceinline__ void store_x(uint16_t* lds, const u32x4_t (&xr)[MF]) {
-#pragma unroll
-  for (int i = 0; i < MF; i++) {
-    const int ci = threadIdx.x + i * 256;
-    const int r = ci >> 3, cc = ci & 7;
-    *(u32x4_t*)(lds + r * kBK + ((cc ^ (r & 7)) << 3)) = xr[i];
-  }
+__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-__device__ __forceinline__ void load_w(const uint16_t* wg, int kt, int lane, u32x4_t (&wr)[8]) {
-  const uint16_t* p = wg + (int64_t)kt * 8 * kFragElems + lane * 8;
-#pragma unroll
-  for (int j = 0; j < 8; j++) wr[j] = *(const u32x4_t*)(p + j * kFragElems);
-}
-
-template <int MF, int EPI, bool PARTIAL>
-__global__ void __launch_bounds__(256) k_gemm(GemmArgs a) {
+// One workgroup: WM x 4 waves. Wave (wm, wn) computes rows
+// [row0 + wm*MF*32, +MF*32) x the 64 packed columns of group tile*4 + wn.
+template <int MF, int WM, int EPI, bool PARTIAL>
+__global__ void __launch_bounds__(256 * WM, 2 / WM) k_gemm(GemmArgs a) {
+  constexpr int NT = 256 * WM;
+  constexpr int BM = WM * MF * 32;
+  constexpr int CPT = BM * 8 / NT;  // 16-byte X chunks per thread per stage (= MF)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   uint16_t* lds0 = smem;
-  uint16_t* lds1 = smem + MF * 32 * kBK;
+  uint16_t* lds1 = smem + BM * kBK;
 
   const int split = blockIdx.x % a.splits;
   const int tile = blockIdx.x / a.splits;
-  const int row0 = blockIdx.y * MF * 32;
+  const int row0 = blockIdx.y * BM;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int ng = tile * kWaves + wave;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int ng = tile * kWaves + wn;
   const bool active = ng < a.NG;
   const int KT = a.KP / kBK;
   const int kt0 = (int)((int64_t)split * KT / a.splits);
   const int kt1 = (int)((int64_t)(split + 1) * KT / a.splits);
-  const uint16_t* wg = a.w + (int64_t)(active ? ng : 0) * (a.KP / 16) * 2 * kFragElems;
+
+  const __amdgpu_buffer_rsrc_t xr_rsrc = make_rsrc(a.x, (uint32_t)((size_t)a.M * a.K * 2));
+  const __amdgpu_buffer_rsrc_t wr_rsrc = make_rsrc(a.w, (uint32_t)((size_t)a.NG * a.KP * 64 * 2));
+  // byte offset of this wave's weight stream: column group ng, 8 fragments (1 KB) per k-tile
+  const uint32_t w_base = (uint32_t)(active ? ng : 0) * (uint32_t)(a.KP / kBK) * 8192u;
+  const uint32_t w_lane = (uint32_t)lane * 16u;
+
+  // X chunks this thread stages: row r, 16-byte column chunk cc of the 64-wide k tile
+  int x_row[CPT], x_cc[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; i++) {
+    const int ci = threadIdx.x + i * NT;
+    x_row[i] = ci >> 3;
+    x_cc[i] = ci & 7;
+  }
 
   f32x16_t acc[MF][2];
 #pragma unroll
@@ -146,41 +149,61 @@ __global__ void __launch_bounds__(256) k_gemm(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; r++) acc[m][n][r] = 0.f;
 
-  u32x4_t xr[MF];
+  u32x4_t xs[CPT];
   u32x4_t wcur[8], wnxt[8];
+
+  auto load_x = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < CPT; i++) {
+      const int row = row0 + x_row[i];
+      const int k = kt * kBK + x_cc[i] * 8;
+      const uint32_t off = (row < a.M && k < a.K) ? (uint32_t)(((size_t)row * a.K + k) * 2) : kOutOfRange;
+      xs[i] = buf_load16(xr_rsrc, off, 0);
+    }
+  };
+  auto store_x = [&](uint16_t* lds) {
+#pragma unroll
+    for (int i = 0; i < CPT; i++) {
+      const int r = x_row[i];
+      *(u32x4_t*)(lds + r * kBK + ((x_cc[i] ^ (r & 7)) << 3)) = xs[i];
+    }
+  };
+  auto load_w = [&](int kt, u32x4_t (&w)[8]) {
+    const uint32_t soff = w_base + (uint32_t)kt * 8192u;
+#pragma unroll
+    for (int j = 0; j < 8; j++) w[j] = buf_load16(wr_rsrc, w_lane + j * 1024u, soff);
+  };
+
   if (kt0 < kt1) {
-    stage_x<MF>(a, row0, kt0, xr);
-    if (active) load_w(wg, kt0, lane, wcur);
-    store_x<MF>(lds0, xr);
+    load_x(kt0);
+    if (active) load_w(kt0, wcur);
+    store_x(lds0);
   }
   __syncthreads();
 
+  const int arow = wm * MF * 32 + (lane & 31);
   for (int kt = kt0; kt < kt1; kt++) {
-    uint16_t* cur = ((kt - kt0) & 1) ? lds1 : lds0;
+    const uint16_t* cur = ((kt - kt0) & 1) ? lds1 : lds0;
     uint16_t* nxt = ((kt - kt0) & 1) ? lds0 : lds1;
     const bool more = kt + 1 < kt1;
     if (more) {
-      stage_x<MF>(a, row0, kt + 1, xr);
-      if (active) load_w(wg, kt + 1, lane, wnxt);
+      load_x(kt + 1);
+      if (active) load_w(kt + 1, wnxt);
     }
     if (active) {
 #pragma unroll
       for (int kb = 0; kb < 4; kb++) {
-        bf16x8_t af[MF];
+        const int cc = kb * 2 + (lane >> 5);
 #pragma unroll
         for (int m = 0; m < MF; m++) {
-          const int r = m * 32 + (lane & 31);
-          const int cc = kb * 2 + (lane >> 5);
-          af[m] = as_bf16x8(*(const u32x4_t*)(cur + r * kBK + ((cc ^ (r & 7)) << 3)));
-        }
-#pragma unroll
-        for (int m = 0; m < MF; m++) {
-          acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], as_bf16x8(wcur[kb * 2 + 0]), acc[m][0], 0, 0, 0);
-          acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], as_bf16x8(wcur[kb * 2 + 1]), acc[m][1], 0, 0, 0);
+          const int r = arow + m * 32;
+          const bf16x8_t af = as_bf16x8(*(const u32x4_t*)(cur + r * kBK + ((cc ^ (r & 7)) << 3)));
+          acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(wcur[kb * 2 + 0]), acc[m][0], 0, 0, 0);
+          acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(wcur[kb * 2 + 1]), acc[m][1], 0, 0, 0);
         }
       }
     }
-    if (more) store_x<MF>(nxt, xr);
+    if (more) store_x(nxt);
     __syncthreads();
     if (more) {
 #pragma unroll
@@ -194,7 +217,7 @@ __global__ void __launch_bounds__(256) k_gemm(GemmArgs a) {
   for (int m = 0; m < MF; m++) {
 #pragma unroll
     for (int r = 0; r < 16; r++) {
-      const int row = row0 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      const int row = row0 + wm * MF * 32 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
       if (row >= a.M) continue;
       if (PARTIAL) {
         float* dst = a.ws + ((int64_t)split * a.M + row) * NP + ng * 64 + (lane & 31);
@@ -263,9 +286,12 @@ int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int mblocks = (M + 255) / 256;
   const int KT = round_up(K, 64) / kBK;
   const int base = tiles * mblocks;
-  int s = (num_cus + base / 2) / base;
+  // Workgroups of up to 128 rows are 4 waves and two fit per CU; 256-row
+  // workgroups are 8 waves, one per CU.
+  const int target = M <= 128 ? 2 * num_cus : num_cus;
+  int s = (target + base / 2) / base;
   if (s < 1) s = 1;
-  if (s > 8) s = 8;
+  if (s > 16) s = 16;
   if (s > KT) s = KT;
   return s;
 }
@@ -292,17 +318,18 @@ hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, voi
   return hipGetLastError();
 }
 
-template <int MF, int EPI, bool P>
+template <int MF, int WM, int EPI, bool P>
 static hipError_t launch_mf(const GemmArgs& a, int mblocks, hipStream_t s) {
-  const size_t lds = (size_t)2 * MF * 32 * kBK * sizeof(uint16_t);
+  const size_t lds = (size_t)2 * WM * MF * 32 * kBK * sizeof(uint16_t);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_gemm<MF, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e =
+        hipFuncSetAttribute((const void*)k_gemm<MF, WM, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   dim3 grid(a.tiles * a.splits, mblocks);
-  k_gemm<MF, EPI, P><<<grid, 256, lds, s>>>(a);
+  k_gemm<MF, WM, EPI, P><<<grid, 256 * WM, lds, s>>>(a);
   return hipGetLastError();
 }
 
@@ -310,10 +337,10 @@ template <int EPI, bool P>
 static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   const int mblocks = (a.M + 255) / 256;
   const int mrows = a.M <= 256 ? a.M : 256;
-  if (mrows <= 32) return launch_mf<1, EPI, P>(a, mblocks, s);
-  if (mrows <= 64) return launch_mf<2, EPI, P>(a, mblocks, s);
-  if (mrows <= 128) return launch_mf<4, EPI, P>(a, mblocks, s);
-  return launch_mf<8, EPI, P>(a, mblocks, s);
+  if (mrows <= 32) return launch_mf<1, 1, EPI, P>(a, mblocks, s);
+  if (mrows <= 64) return launch_mf<2, 1, EPI, P>(a, mblocks, s);
+  if (mrows <= 128) return launch_mf<4, 1, EPI, P>(a, mblocks, s);
+  return launch_mf<4, 2, EPI, P>(a, mblocks, s);
 }
 
 hipError_t launch_linear(const LinearCall& c, hipStream_t s) {

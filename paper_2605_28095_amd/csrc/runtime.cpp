@@ -129,6 +129,14 @@ struct sidp_handle {
   int copy_grid = 512;
   hipStream_t last_compute = nullptr, last_copy = nullptr;
   bool any_copy = false;
+  // SIDP_TIMING: event pairs per kernel class launch, recycled by sidp_timing_collect
+  struct TimedPair {
+    int cls;
+    hipEvent_t a, b;
+  };
+  std::vector<hipEvent_t> event_pool;
+  std::vector<TimedPair> timed;
+  bool timing = false;
 };
 
 #define HIPCHK(h, expr)                \
@@ -170,6 +178,11 @@ static void free_device(sidp_handle* h) {
     if (h->filled[i]) (void)hipEventDestroy(h->filled[i]);
     if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
   }
+  for (auto& t : h->timed) {
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
 }
 
 int sidp_create(const sidp_config* cfg, sidp_handle** out) {
@@ -383,19 +396,47 @@ static LinearCall linear_call(const sidp_handle* h, const void* x, int m, int k,
   return c;
 }
 
+// SIDP_TIMING: open a timed interval of kernel class `cls` on stream s.
+static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
+  if (!h->timing) return hipSuccess;
+  hipEvent_t ev[2];
+  for (int i = 0; i < 2; i++) {
+    if (!h->event_pool.empty()) {
+      ev[i] = h->event_pool.back();
+      h->event_pool.pop_back();
+    } else {
+      hipError_t e = hipEventCreate(&ev[i]);
+      if (e != hipSuccess) return e;
+    }
+  }
+  h->timed.push_back({cls, ev[0], ev[1]});
+  return hipEventRecord(ev[0], s);
+}
+static hipError_t time_end(sidp_handle* h, hipStream_t s) {
+  if (!h->timing) return hipSuccess;
+  return hipEventRecord(h->timed.back().b, s);
+}
+
+#define TIMED(h, cls, s, expr)                                      \
+  do {                                                              \
+    hipError_t te_;                                                 \
+    if ((te_ = time_begin((h), (cls), (s))) != hipSuccess) return te_; \
+    if ((te_ = (expr)) != hipSuccess) return te_;                   \
+    if ((te_ = time_end((h), (s))) != hipSuccess) return te_;       \
+  } while (0)
+
 // The per-layer kernel sequence, reading weights from `wb` (a pool blob or a slot).
 static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, const int32_t* positions,
                             const int32_t* bt, int max_blocks, int B, hipStream_t s) {
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, D = c.head_dim, QD = c.num_q_heads * D;
-  hipError_t e;
   // a2: RMSNorm before attention
-  if ((e = launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s)) != hipSuccess) return e;
+  TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
   // a3: QKV projection (+ bias)
-  if ((e = launch_linear(linear_call(h, h->h, B, H, wb + L.w_qkv, qkv_rows(c), SIDP_EPI_BF16,
-                                     c.qkv_bias ? wb + L.bias : nullptr, nullptr, h->qkv), s)) != hipSuccess)
-    return e;
+  TIMED(h, SIDP_K_QKV, s,
+        launch_linear(linear_call(h, h->h, B, H, wb + L.w_qkv, qkv_rows(c), SIDP_EPI_BF16,
+                                  c.qkv_bias ? wb + L.bias : nullptr, nullptr, h->qkv), s));
   // a4/a5: QK-norm, RoPE, KV append at the slot of each sequence's position
   RopeCall r;
   r.qkv = h->qkv;
@@ -416,7 +457,7 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   r.region = layer % h->regions;
   r.q_out = h->q;
   r.err = h->err;
-  if ((e = launch_rope_append(r, s)) != hipSuccess) return e;
+  TIMED(h, SIDP_K_ROPE, s, launch_rope_append(r, s));
   // a6: paged GQA attention
   AttnCall a;
   a.q = h->q;
@@ -433,19 +474,21 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   a.part = h->attn_part;
   a.max_parts = h->attn_max_parts;
   a.err = h->err;
-  if ((e = launch_attention(a, s)) != hipSuccess) return e;
+  TIMED(h, SIDP_K_ATTN, s, launch_attention(a, s));
   // a7: O projection + residual (in place on the fp32 residual stream)
-  if ((e = launch_linear(linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s)) !=
-      hipSuccess)
-    return e;
+  TIMED(h, SIDP_K_O, s,
+        launch_linear(linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s));
   // a8: RMSNorm before the FFN
-  if ((e = launch_rmsnorm(hidden, wb + L.g_mlp, c.rms_eps, h->h, B, H, s)) != hipSuccess) return e;
+  TIMED(h, SIDP_K_NORM_MLP, s, launch_rmsnorm(hidden, wb + L.g_mlp, c.rms_eps, h->h, B, H, s));
   // a9: gate/up projection + SwiGLU
-  if ((e = launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
-                         s)) != hipSuccess)
-    return e;
+  TIMED(h, SIDP_K_GATE_UP, s,
+        launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
+                      s));
   // a10: down projection + residual
-  return launch_linear(linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s);
+  TIMED(h, SIDP_K_DOWN, s,
+        launch_linear(linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden),
+                      s));
+  return hipSuccess;
 }
 
 // One slot fill on the copy stream: layer (g mod L) from the pool into `slot`.
@@ -458,9 +501,11 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, int flags, hip
     if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
   if (flags & SIDP_DEBUG_DELAY)
     if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
+  if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst, src, lb, hipMemcpyDeviceToDevice, cp);
   else e = launch_copy(src, dst, lb, h->copy_grid, cp);
   if (e != hipSuccess) return e;
+  if ((e = time_end(h, cp)) != hipSuccess) return e;
   return hipEventRecord(h->filled[slot], cp);
 }
 
@@ -477,6 +522,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   const int parts = (max_blocks_per_seq * c.block_size + attn_part_tokens() - 1) / attn_part_tokens();
   if (parts > h->attn_max_parts) return SIDP_EINVAL;
   const bool streamed = flags & SIDP_STREAMED;
+  h->timing = (flags & SIDP_TIMING) != 0;
   hipStream_t cs = (hipStream_t)compute, cp = (hipStream_t)copy;
   if (streamed && (!h->slots || cp == cs)) return SIDP_EINVAL;
   h->last_compute = cs;
@@ -501,7 +547,12 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
     const int64_t g = h->ring_g++;
     ring_layer(g, copy_ops, compute_ops);
     for (RingOp& op : compute_ops) {
-      if (op.kind == OP_WAIT_FILL) HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
+      if (op.kind == OP_WAIT_FILL) {
+        // under SIDP_TIMING the interval around the wait is the compute stall on the fill
+        HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
+        HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
+        HIPCHK(h, time_end(h, cs));
+      }
       else if (op.kind == OP_COMPUTE)
         HIPCHK(h, run_layer(h, h->slots + (size_t)op.slot * h->blob.total, (int)(op.g % c.num_layers), hidden,
                             positions, block_tables, max_blocks_per_seq, batch, cs));
@@ -529,6 +580,26 @@ int sidp_sync(sidp_handle* h) {
     HIPCHK(h, hipMemset(h->err, 0, 4));
     return SIDP_EINVAL;
   }
+  return SIDP_OK;
+}
+
+int sidp_timing_collect(sidp_handle* h, double* ms, int32_t* launches) {
+  if (!h || !ms || !launches) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  for (int i = 0; i < SIDP_NUM_KCLASSES; i++) {
+    ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  for (auto& t : h->timed) {
+    HIPCHK(h, hipEventSynchronize(t.b));
+    float el = 0.f;
+    HIPCHK(h, hipEventElapsedTime(&el, t.a, t.b));
+    ms[t.cls] += el;
+    launches[t.cls]++;
+    h->event_pool.push_back(t.a);
+    h->event_pool.push_back(t.b);
+  }
+  h->timed.clear();
   return SIDP_OK;
 }
 
