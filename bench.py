@@ -97,7 +97,7 @@ def main():
     ap.add_argument("--workload", default="llama70b_stack80")
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--mode", choices=["streamed", "resident"], default="streamed")
-    ap.add_argument("--copy", choices=["kernel", "memcpy"], default="kernel")
+    ap.add_argument("--copy", choices=["background", "burst", "memcpy"], default="background")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -185,6 +185,8 @@ def main():
     flags = sidp.SIDP_STREAMED if args.mode == "streamed" else sidp.SIDP_RESIDENT
     if args.copy == "memcpy":
         flags |= sidp.SIDP_COPY_MEMCPY
+    elif args.copy == "burst":
+        flags |= sidp.SIDP_COPY_BURST
 
     for i in range(args.warmup):
         dec.step(hidden, pos, bt, flags, compute=compute, copy=copy_stream)

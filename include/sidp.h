@@ -53,7 +53,9 @@ extern "C" {
 /* ---- sidp_decode_step flags ---- */
 #define SIDP_RESIDENT      0x0  /* each layer computes straight from its pool blob */
 #define SIDP_STREAMED      0x1  /* layers stream through the 2-slot cache ring */
-#define SIDP_COPY_MEMCPY   0x2  /* slot fills by hipMemcpyAsync (default: library copy kernel) */
+#define SIDP_COPY_MEMCPY   0x2  /* slot fills by hipMemcpyAsync                                  */
+#define SIDP_COPY_BURST    0x4  /* slot fills by a full-grid copy kernel                         */
+                                /* default: a background fill kernel sized to run beside compute */
 #define SIDP_DEBUG_POISON  0x10 /* before each fill, write NaN bytes over the slot */
 #define SIDP_DEBUG_DELAY   0x20 /* before each fill, spin ~200 us on the copy stream */
 #define SIDP_TIMING        0x40 /* bracket each kernel class with HIP events (sidp_timing_collect) */

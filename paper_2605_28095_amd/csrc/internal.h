@@ -71,12 +71,14 @@ struct AttnCall {
   float* part;        // partials [B][Hq][max_parts][D + 2]
   int max_parts;
   uint32_t* err;
+  int num_cus;
 };
 int attn_part_tokens();
 size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq);
 hipError_t launch_attention(const AttnCall& c, hipStream_t s);
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);
+hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s);
 hipError_t launch_poison(void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_spin(int64_t cycles, hipStream_t s);
 

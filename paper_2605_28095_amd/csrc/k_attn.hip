@@ -1,26 +1,28 @@
 // Paged grouped-query decode attention on gfx950 (K4).
 //
-// Work item: (sequence b, KV head g, 512-token partition); 4 waves, 128
-// tokens each, in chunks of 32 tokens = two 16-token KV blocks. The query
-// heads of a KV group (up to 16) ride in the MFMA's 16 columns, so every KV
-// byte is read once for all heads of its group:
-//   S^T[token][head] = K[token][:] . Q^T[:][head]   (v_mfma_f32_16x16x32_bf16,
-//                                                    A = K rows straight from the block)
+// Work is a flat list of items (sequence b, partition p, KV head g), a
+// partition being 1024 tokens; a persistent grid of 4-wave workgroups walks
+// the list. Within an item each wave owns 256 tokens, processed in chunks of
+// 32 tokens = two 16-token KV blocks, with the next chunk's K/V loads in
+// flight while the current one computes. The query heads of a KV group (up to
+// 16) ride in the MFMA's 16 columns, so every KV byte is read once for all of
+// them:
+//   S^T[token][head] = K[token][:] . Q^T[:][head]   (v_mfma_f32_16x16x32_bf16)
 //   O^T[dim][head]  += V^T[dim][token] . P[token][head]
-// V blocks are stored transposed ([d][token]) so V^T fragments are 8-byte
-// row pieces; the MFMA's k order of tokens is permuted identically on P and
-// V^T so that the softmax probabilities never leave the lanes that computed
-// them. Softmax is online (running max, rescale) in base-2 units; partitions
-// of one (b, g) are merged in LDS and, when a sequence spans several
-// partitions, by a log-sum-exp combine kernel. Fixed reduction order: the
-// result does not depend on scheduling.
+// V blocks are stored transposed ([d][token]) so V^T fragments are 8-byte row
+// pieces; the MFMA's k order of tokens is permuted identically on P and V^T so
+// that the softmax probabilities never leave the lanes that computed them. P
+// is split into high and low bf16 parts (two MFMAs), keeping the product at
+// fp32-like accuracy. Softmax is online in base-2 units; the four waves of an
+// item are merged in LDS; a sequence spanning several partitions is merged
+// by a log-sum-exp combine kernel. Every reduction has a fixed order.
 #include "common.h"
 #include "internal.h"
 
 namespace sidp {
 
-constexpr int kPartTokens = 512;
-constexpr int kWaveTokens = 128;
+constexpr int kPartTokens = 1024;
+constexpr int kWaveTokens = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 int attn_part_tokens() { return kPartTokens; }
@@ -31,178 +33,240 @@ size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq) {
 }
 
 template <int D>
-__global__ void __launch_bounds__(256) k_attn(AttnCall a) {
-  constexpr int KK = D / 32;   // k steps of the QK product
-  constexpr int JD = D / 16;   // 16-dim column tiles of the PV product
-  __shared__ float s_m[4][16], s_l[4][16];
-  __shared__ float s_o[4][16][D + 1];
+struct Chunk {
+  u32x4_t k[2][D / 32];  // K fragments: token lane&15, dims (lane>>4)*8 + 32kk
+  u32x2_t v[D / 16][2];  // V^T fragments: dim 16jd + lane&15, tokens (lane>>4)*4..+3
+};
 
-  const int b = blockIdx.z, g = blockIdx.y, part = blockIdx.x;
-  const int seq = a.positions[b] + 1;
-  if (seq < 1 || seq > a.max_blocks * a.kv.bs) {  // position outside its block table
-    if (part == 0 && g == 0 && threadIdx.x == 0) atomicOr(a.err, SIDP_DEVERR_POSITION);
-    return;
-  }
-  const int nparts = (seq + kPartTokens - 1) / kPartTokens;
-  if (part >= nparts) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int group = a.hq / a.hkv;
+template <int D>
+__device__ __forceinline__ void load_chunk(const AttnCall& a, const int32_t* bt, int64_t region_blk, int g, int t0,
+                                           int seq, int lane, Chunk<D>& c) {
+  constexpr int KK = D / 32, JD = D / 16;
   const int head = lane & 15, lg = lane >> 4;
-
-  // Q^T as the B operand: lane holds dims lg*8..lg*8+7 (+32 kk) of head `head`.
-  bf16x8_t qb[KK];
+  int blk[2];
+  blk[0] = bt[t0 >> 4];
+  blk[1] = (t0 + 16 < seq) ? bt[(t0 >> 4) + 1] : blk[0];
 #pragma unroll
-  for (int kk = 0; kk < KK; kk++) {
-    u32x4_t v = {0u, 0u, 0u, 0u};
-    if (head < group) v = *(const u32x4_t*)(a.q + ((int64_t)b * a.hq + g * group + head) * D + lg * 8 + kk * 32);
-    qb[kk] = as_bf16x8(v);
+  for (int j = 0; j < 2; j++) {
+    if (blk[j] < 0 || blk[j] >= a.kv.nblk) {
+      if (lane == 0) atomicOr(a.err, SIDP_DEVERR_BLOCK);
+      blk[j] = 0;
+    }
   }
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    const uint16_t* kp = a.kv.k + (((region_blk + blk[j]) * a.kv.hkv + g) * 16 + head) * D + lg * 8;
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = *(const u32x4_t*)(kp + kk * 32);
+    const uint16_t* vp = a.kv.v + ((region_blk + blk[j]) * a.kv.hkv + g) * (int64_t)D * 16 + lg * 4;
+#pragma unroll
+    for (int jd = 0; jd < JD; jd++) c.v[jd][j] = *(const u32x2_t*)(vp + (jd * 16 + head) * 16);
+  }
+}
 
-  const int t_begin = part * kPartTokens + wave * kWaveTokens;
-  const int t_end = min(t_begin + kWaveTokens, seq);
-  const float scale = kLog2e / sqrtf((float)D);
-  const int64_t region_blk = (int64_t)a.region * a.kv.nblk;
-  const int32_t* bt = a.block_tables + (int64_t)b * a.max_blocks;
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t o[JD];
+template <int D>
+__device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t (&qb)[D / 32], int t0, int seq,
+                                              int lane, float scale, float& m_run, float& l_run,
+                                              f32x4_t (&o)[D / 16]) {
+  constexpr int KK = D / 32, JD = D / 16;
+  const int lg = lane >> 4;
+  f32x4_t s[2];
 #pragma unroll
-  for (int j = 0; j < JD; j++) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int t0 = t_begin; t0 < t_end; t0 += 32) {
-    const int lb0 = t0 / 16;
-    int blk[2];
-    blk[0] = bt[lb0];
-    blk[1] = (t0 + 16 < seq) ? bt[lb0 + 1] : blk[0];
+  for (int j = 0; j < 2; j++) {
+    s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 2; j++) {
-      if (blk[j] < 0 || blk[j] >= a.kv.nblk) {
-        if (lane == 0) atomicOr(a.err, SIDP_DEVERR_BLOCK);
-        blk[j] = 0;
-      }
-    }
-    // K fragments (A operand): token lane&15 of block j, dims lg*8 + 32kk.
-    u32x4_t kf[2][KK];
+    for (int kk = 0; kk < KK; kk++)
+      s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(c.k[j][kk]), qb[kk], s[j], 0, 0, 0);
+  }
+  const bool tail = t0 + 32 > seq;
+  float cmax = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 2; j++) {
-      const uint16_t* kp = a.kv.k + (((region_blk + blk[j]) * a.kv.hkv + g) * 16 + head) * D + lg * 8;
-#pragma unroll
-      for (int kk = 0; kk < KK; kk++) kf[j][kk] = *(const u32x4_t*)(kp + kk * 32);
-    }
-    // V^T fragments (A operand of PV): dim 16jd + lane&15, tokens lg*4..lg*4+3 of each block.
-    u32x2_t vf[JD][2];
-#pragma unroll
-    for (int j = 0; j < 2; j++) {
-      const uint16_t* vp = a.kv.v + ((region_blk + blk[j]) * a.kv.hkv + g) * (int64_t)D * 16 + lg * 4;
-#pragma unroll
-      for (int jd = 0; jd < JD; jd++) vf[jd][j] = *(const u32x2_t*)(vp + (jd * 16 + head) * 16);
-    }
-
-    f32x4_t s[2];
-#pragma unroll
-    for (int j = 0; j < 2; j++) {
-      s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KK; kk++)
-        s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[j][kk]), qb[kk], s[j], 0, 0, 0);
-    }
-    // scale, mask, chunk max per head
-    float cmax = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 2; j++)
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        const int t = t0 + 16 * j + lg * 4 + r;
-        float v = s[j][r] * scale;
-        v = (t < seq) ? v : -INFINITY;
-        s[j][r] = v;
-        cmax = fmaxf(cmax, v);
-      }
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
-    const float m_new = fmaxf(m_run, cmax);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    // Probabilities enter the bf16 MFMA as a high and a low bf16 part
-    // (p = hi + lo to about 16 significant bits), so P.V is as accurate as
-    // an fp32 product; attention is HBM-bound and the second MFMA is free.
-    float psum = 0.f;
-    float p[8];
+  for (int j = 0; j < 2; j++)
 #pragma unroll
     for (int r = 0; r < 4; r++) {
-      p[r] = exp2f(s[0][r] - m_new);      // slots 0..3: block 0 tokens lg*4 + r
-      p[4 + r] = exp2f(s[1][r] - m_new);  // slots 4..7: block 1 tokens lg*4 + r
-      psum += p[r] + p[4 + r];
+      float v = s[j][r] * scale;
+      if (tail && t0 + 16 * j + lg * 4 + r >= seq) v = -INFINITY;
+      s[j][r] = v;
+      cmax = fmaxf(cmax, v);
     }
-    l_run = l_run * alpha + psum;
-    uint32_t hi[4], lo[4];
+  cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
+  cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+  const float m_new = fmaxf(m_run, cmax);
+  const float alpha = exp2f(m_run - m_new);
+  m_run = m_new;
+  float p[8];
+  float psum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const uint16_t h0 = f2bf(p[2 * i]), h1 = f2bf(p[2 * i + 1]);
-      hi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-      lo[i] = pack_bf2(p[2 * i] - bf2f(h0), p[2 * i + 1] - bf2f(h1));
-    }
-    const bf16x8_t pb = as_bf16x8(u32x4_t{hi[0], hi[1], hi[2], hi[3]});
-    const bf16x8_t pl = as_bf16x8(u32x4_t{lo[0], lo[1], lo[2], lo[3]});
-    const bool tail = t0 + 32 > seq;
-#pragma unroll
-    for (int jd = 0; jd < JD; jd++) {
-      u32x2_t v0 = vf[jd][0], v1 = vf[jd][1];
-      if (tail) {  // invalid tokens may hold anything (NaN); zero them so 0 * V stays 0
-        const int tb = t0 + lg * 4;
-        if (tb + 0 >= seq) v0.x &= 0xffff0000u;
-        if (tb + 1 >= seq) v0.x &= 0x0000ffffu;
-        if (tb + 2 >= seq) v0.y &= 0xffff0000u;
-        if (tb + 3 >= seq) v0.y &= 0x0000ffffu;
-        if (tb + 16 >= seq) v1.x &= 0xffff0000u;
-        if (tb + 17 >= seq) v1.x &= 0x0000ffffu;
-        if (tb + 18 >= seq) v1.y &= 0xffff0000u;
-        if (tb + 19 >= seq) v1.y &= 0x0000ffffu;
-      }
-      const bf16x8_t va = as_bf16x8(u32x4_t{v0.x, v0.y, v1.x, v1.y});
-      o[jd] = o[jd] * alpha;
-      o[jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[jd], 0, 0, 0);
-      o[jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, o[jd], 0, 0, 0);
-    }
+  for (int r = 0; r < 4; r++) {
+    p[r] = exp2f(s[0][r] - m_new);      // slots 0..3: block 0 tokens lg*4 + r
+    p[4 + r] = exp2f(s[1][r] - m_new);  // slots 4..7: block 1 tokens lg*4 + r
+    psum += p[r] + p[4 + r];
   }
-  // l over the four lane groups holding different tokens of the same head
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
+  l_run = l_run * alpha + psum;
+  // P as high + low bf16 parts
+  uint32_t hi[4], lo[4];
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    hi[i] = pack_bf2(p[2 * i], p[2 * i + 1]);
+    lo[i] = pack_bf2(p[2 * i] - bf2f((uint16_t)(hi[i] & 0xffffu)), p[2 * i + 1] - bf2f((uint16_t)(hi[i] >> 16)));
+  }
+  const bf16x8_t pb = as_bf16x8(u32x4_t{hi[0], hi[1], hi[2], hi[3]});
+  const bf16x8_t pl = as_bf16x8(u32x4_t{lo[0], lo[1], lo[2], lo[3]});
+#pragma unroll
+  for (int jd = 0; jd < JD; jd++) {
+    u32x2_t v0 = c.v[jd][0], v1 = c.v[jd][1];
+    if (tail) {  // invalid tokens may hold anything (NaN); zero them so 0 * V stays 0
+      const int tb = t0 + lg * 4;
+      if (tb + 0 >= seq) v0.x &= 0xffff0000u;
+      if (tb + 1 >= seq) v0.x &= 0x0000ffffu;
+      if (tb + 2 >= seq) v0.y &= 0xffff0000u;
+      if (tb + 3 >= seq) v0.y &= 0x0000ffffu;
+      if (tb + 16 >= seq) v1.x &= 0xffff0000u;
+      if (tb + 17 >= seq) v1.x &= 0x0000ffffu;
+      if (tb + 18 >= seq) v1.y &= 0xffff0000u;
+      if (tb + 19 >= seq) v1.y &= 0x0000ffffu;
+    }
+    const bf16x8_t va = as_bf16x8(u32x4_t{v0.x, v0.y, v1.x, v1.y});
+    o[jd] = o[jd] * alpha;
+    o[jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[jd], 0, 0, 0);
+    o[jd] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, o[jd], 0, 0, 0);
+  }
+}
 
-  if (lg == 0) {
-    s_m[wave][head] = m_run;
-    s_l[wave][head] = l_run;
+__device__ __forceinline__ int seq_parts(const AttnCall& a, int b) {
+  const int seq = a.positions[b] + 1;
+  if (seq < 1 || seq > a.max_blocks * a.kv.bs) return 0;  // position outside its block table
+  return (seq + kPartTokens - 1) / kPartTokens;
+}
+
+// Items of sequence b are prefix[b] * Hkv .. prefix[b+1] * Hkv - 1, ordered
+// (partition, KV head); prefix[] is built in LDS once per workgroup.
+template <int D>
+__global__ void __launch_bounds__(256, 2) k_attn(AttnCall a) {
+  constexpr int KK = D / 32, JD = D / 16;
+  extern __shared__ __attribute__((aligned(16))) float smem_f[];
+  float* s_m = smem_f;                             // [4][16]
+  float* s_l = s_m + 64;                           // [4][16]
+  float* s_o = s_l + 64;                           // [4][16][D + 1]
+  int* s_prefix = (int*)(s_o + 4 * 16 * (D + 1));  // [batch + 1]
+  __shared__ int s_scan[256];
+
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int head = lane & 15, lg = lane >> 4;
+  const int group = a.hq / a.hkv;
+  const int B = a.batch;
+
+  // Exclusive prefix over sequences of their partition counts. Thread t owns
+  // sequences [t*per, t*per + per).
+  const int per = (B + 255) / 256;
+  int local = 0;
+  for (int i = 0; i < per; i++) {
+    const int b = threadIdx.x * per + i;
+    if (b < B) {
+      const int n = seq_parts(a, b);
+      if (n == 0 && blockIdx.x == 0) atomicOr(a.err, SIDP_DEVERR_POSITION);
+      local += n;
+    }
   }
-#pragma unroll
-  for (int jd = 0; jd < JD; jd++)
-#pragma unroll
-    for (int r = 0; r < 4; r++) s_o[wave][head][jd * 16 + lg * 4 + r] = o[jd][r];
+  s_scan[threadIdx.x] = local;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {  // inclusive scan
+    const int v = threadIdx.x >= off ? s_scan[threadIdx.x - off] : 0;
+    __syncthreads();
+    s_scan[threadIdx.x] += v;
+    __syncthreads();
+  }
+  int run = s_scan[threadIdx.x] - local;
+  for (int i = 0; i < per; i++) {
+    const int b = threadIdx.x * per + i;
+    if (b < B) {
+      s_prefix[b] = run;
+      run += seq_parts(a, b);
+    }
+  }
+  if (threadIdx.x == 0) s_prefix[B] = s_scan[255];
   __syncthreads();
 
-  // Merge the four waves: thread -> (head, dim) pairs of this group.
-  for (int i = threadIdx.x; i < group * D; i += 256) {
-    const int hh = i / D, d = i % D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w][hh]);
-    float L = 0.f, O = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; w++) {
-      const float f = (s_m[w][hh] == -INFINITY) ? 0.f : exp2f(s_m[w][hh] - M);
-      L += s_l[w][hh] * f;
-      O += s_o[w][hh][d] * f;
+  const int total_items = s_prefix[B] * a.hkv;
+  const float scale = kLog2e / sqrtf((float)D);
+  const int64_t region_blk = (int64_t)a.region * a.kv.nblk;
+
+  for (int item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int pg = item / a.hkv, g = item % a.hkv;
+    int lo_b = 0, hi_b = B - 1;  // last b with prefix[b] <= pg
+    while (lo_b < hi_b) {
+      const int mid = (lo_b + hi_b + 1) >> 1;
+      if (s_prefix[mid] <= pg) lo_b = mid;
+      else hi_b = mid - 1;
     }
-    const int qh = g * group + hh;
-    if (nparts == 1) {
-      a.out[((int64_t)b * a.hq + qh) * D + d] = f2bf(O / L);
-    } else {
-      float* p = a.part + (((int64_t)b * a.hq + qh) * a.max_parts + part) * (D + 2);
-      p[d] = O;
-      if (d == 0) {
-        p[D] = M;
-        p[D + 1] = L;
+    const int b = lo_b;
+    const int part = pg - s_prefix[b];
+    const int nparts = s_prefix[b + 1] - s_prefix[b];
+    const int seq = a.positions[b] + 1;
+    const int32_t* bt = a.block_tables + (int64_t)b * a.max_blocks;
+
+    bf16x8_t qb[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++) {
+      u32x4_t v = {0u, 0u, 0u, 0u};
+      if (head < group) v = *(const u32x4_t*)(a.q + ((int64_t)b * a.hq + g * group + head) * D + lg * 8 + kk * 32);
+      qb[kk] = as_bf16x8(v);
+    }
+    const int t_begin = part * kPartTokens + wave * kWaveTokens;
+    const int t_end = min(t_begin + kWaveTokens, seq);
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4_t o[JD];
+#pragma unroll
+    for (int j = 0; j < JD; j++) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // chunks of 32 tokens, two register buffers: load the next while computing one
+    Chunk<D> ca, cb;
+    if (t_begin < t_end) load_chunk<D>(a, bt, region_blk, g, t_begin, seq, lane, ca);
+    for (int t0 = t_begin; t0 < t_end; t0 += 64) {
+      const int t1 = t0 + 32;
+      if (t1 < t_end) load_chunk<D>(a, bt, region_blk, g, t1, seq, lane, cb);
+      compute_chunk<D>(ca, qb, t0, seq, lane, scale, m_run, l_run, o);
+      if (t1 + 32 < t_end) load_chunk<D>(a, bt, region_blk, g, t1 + 32, seq, lane, ca);
+      if (t1 < t_end) compute_chunk<D>(cb, qb, t1, seq, lane, scale, m_run, l_run, o);
+    }
+    l_run += __shfl_xor(l_run, 16, 64);
+    l_run += __shfl_xor(l_run, 32, 64);
+
+    if (lg == 0) {
+      s_m[wave * 16 + head] = m_run;
+      s_l[wave * 16 + head] = l_run;
+    }
+#pragma unroll
+    for (int jd = 0; jd < JD; jd++)
+#pragma unroll
+      for (int r = 0; r < 4; r++) s_o[(wave * 16 + head) * (D + 1) + jd * 16 + lg * 4 + r] = o[jd][r];
+    __syncthreads();
+    for (int i = threadIdx.x; i < group * D; i += 256) {
+      const int hh = i / D, d = i % D;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
+      float L = 0.f, O = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; w++) {
+        const float mw = s_m[w * 16 + hh];
+        const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+        L += s_l[w * 16 + hh] * f;
+        O += s_o[(w * 16 + hh) * (D + 1) + d] * f;
+      }
+      const int qh = g * group + hh;
+      if (nparts == 1) {
+        a.out[((int64_t)b * a.hq + qh) * D + d] = f2bf(O / L);
+      } else {
+        float* pp = a.part + (((int64_t)b * a.hq + qh) * a.max_parts + part) * (D + 2);
+        pp[d] = O;
+        if (d == 0) {
+          pp[D] = M;
+          pp[D + 1] = L;
+        }
       }
     }
+    __syncthreads();  // s_m, s_l and s_o are reused by the next item
   }
 }
 
@@ -210,9 +274,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnCall a) {
 template <int D>
 __global__ void __launch_bounds__(D) k_attn_combine(AttnCall a) {
   const int qh = blockIdx.x, b = blockIdx.y;
-  const int seq = a.positions[b] + 1;
-  if (seq < 1 || seq > a.max_blocks * a.kv.bs) return;
-  const int nparts = (seq + kPartTokens - 1) / kPartTokens;
+  const int nparts = seq_parts(a, b);
   if (nparts <= 1) return;
   const float* p = a.part + ((int64_t)b * a.hq + qh) * a.max_parts * (D + 2);
   float M = -INFINITY;
@@ -227,21 +289,27 @@ __global__ void __launch_bounds__(D) k_attn_combine(AttnCall a) {
   a.out[((int64_t)b * a.hq + qh) * D + d] = f2bf(O / L);
 }
 
+template <int D>
+static hipError_t launch_d(const AttnCall& c, int grid, int parts, hipStream_t s) {
+  const size_t lds = (size_t)(128 + 4 * 16 * (D + 1)) * 4 + (size_t)(c.batch + 1) * 4;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_attn<D>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  k_attn<D><<<grid, 256, lds, s>>>(c);
+  if (parts > 1) k_attn_combine<D><<<dim3(c.hq, c.batch), D, 0, s>>>(c);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const AttnCall& c, hipStream_t s) {
   if (c.batch <= 0) return hipSuccess;
   const int parts = (c.max_blocks * c.kv.bs + kPartTokens - 1) / kPartTokens;
   if (parts > c.max_parts) return hipErrorInvalidValue;
-  dim3 grid(parts, c.hkv, c.batch);
-  if (c.d == 128) {
-    k_attn<128><<<grid, 256, 0, s>>>(c);
-    if (parts > 1) k_attn_combine<128><<<dim3(c.hq, c.batch), 128, 0, s>>>(c);
-  } else if (c.d == 64) {
-    k_attn<64><<<grid, 256, 0, s>>>(c);
-    if (parts > 1) k_attn_combine<64><<<dim3(c.hq, c.batch), 64, 0, s>>>(c);
-  } else {
-    return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  if (c.hq / c.hkv > 16) return hipErrorInvalidValue;
+  const int grid = 2 * c.num_cus;  // persistent: two 4-wave workgroups per CU
+  if (c.d == 128) return launch_d<128>(c, grid, parts, s);
+  if (c.d == 64) return launch_d<64>(c, grid, parts, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace sidp

@@ -28,6 +28,50 @@ __global__ void __launch_bounds__(256) k_copy16(const f4v_t* __restrict__ src, f
   for (; i < n; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
+// Background slot fill: runs beside the layer kernels instead of ahead of
+// them. One 4-wave workgroup per CU, at most 16 VGPRs per wave, scalar buffer
+// bases: a fill wave fits in the registers a projection or attention SIMD
+// leaves free (2 x 248 + 16 = 512). The 81 KB of LDS it requests and never
+// touches keeps two fill workgroups off one CU (2 x 81 KB > 160 KB) while one
+// still fits beside two projection (2 x 32 KB) or two attention (2 x 36 KB)
+// workgroups, so the fill never claims the resources a layer kernel needs.
+constexpr int kFillLdsBytes = 81 * 1024;
+constexpr uint32_t kFillRsrcWord3 = 0x00020000u;
+
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(16)))
+k_fill_bg(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
+  extern __shared__ uint8_t fill_lds_reserve[];
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(src), (short)0,
+                                                                      (int)(n16 * 16u), (int)kFillRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(dst, (short)0, (int)(n16 * 16u),
+                                                                      (int)kFillRsrcWord3);
+  const uint32_t stride = gridDim.x * 256u;
+  uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  for (; i + stride < n16; i += 2 * stride) {
+    const f4v_t a = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16u, 0, 2));
+    const f4v_t b = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (i + stride) * 16u, 0, 2));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, a), rd, i * 16u, 0, 2);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, b), rd, (i + stride) * 16u, 0, 2);
+  }
+  if (i < n16) {
+    const f4v_t a = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16u, 0, 2));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, a), rd, i * 16u, 0, 2);
+  }
+}
+
+hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if (bytes % 16 || bytes >= ((size_t)1 << 31)) return launch_copy(src, dst, bytes, 0, s);
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_fill_bg, hipFuncAttributeMaxDynamicSharedMemorySize, kFillLdsBytes);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  k_fill_bg<<<num_cus, 256, kFillLdsBytes, s>>>((const uint8_t*)src, (uint8_t*)dst, (uint32_t)(bytes / 16));
+  return hipGetLastError();
+}
+
 __global__ void k_copy_tail(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, size_t n) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[i];

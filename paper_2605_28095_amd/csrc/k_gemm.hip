@@ -10,8 +10,10 @@
 //    group streams its weights with 1 KB fully contiguous loads straight
 //    into registers; no LDS traffic for W.
 //  * Activations X are shared by the 4 waves of a workgroup: staged through
-//    LDS (64-wide k tiles, double buffered, 16-byte chunks XOR-swizzled by
-//    row so fragment reads spread over the banks).
+//    LDS (64-wide k tiles, double buffered). A row is 128 bytes; its 16-byte
+//    chunk c is stored at slot c ^ ((row >> 1) & 7), so the 16 lanes that one
+//    LDS cycle serves for a 128-bit fragment read (rows r..r+15, one chunk)
+//    hit 16 distinct 16-byte bank groups of the 64 four-byte banks.
 //  * A workgroup covers up to 256 rows x 256 columns with 4 or 8 waves; each
 //    wave holds MF x 2 accumulators of 32x32 (up to 128 rows x 64 columns)
 //    and issues v_mfma_f32_32x32x16_bf16; two waves share each SIMD.
@@ -21,6 +23,8 @@
 //    tiles), K is split; each split writes fp32 partials and a reduction
 //    kernel sums them in split order (deterministic, so streamed and resident
 //    runs are bit-identical) and applies the epilogue.
+#include <cstdlib>
+
 #include "common.h"
 #include "internal.h"
 
@@ -85,6 +89,7 @@ struct GemmArgs {
   int tiles;           // ceil(NG / kWaves)
   int splits;
   int N;               // valid output columns (SWIGLU: F)
+  int mblocks;         // row blocks of BM rows
   void* out;
   const uint16_t* bias;  // EPI_BF16
   const float* resid;    // EPI_RESID
@@ -107,7 +112,7 @@ __device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t
 // One workgroup: WM x 4 waves. Wave (wm, wn) computes rows
 // [row0 + wm*MF*32, +MF*32) x the 64 packed columns of group tile*4 + wn.
 template <int MF, int WM, int EPI, bool PARTIAL>
-__global__ void __launch_bounds__(256 * WM, 2 / WM) k_gemm(GemmArgs a) {
+__global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm(GemmArgs a) {
   constexpr int NT = 256 * WM;
   constexpr int BM = WM * MF * 32;
   constexpr int CPT = BM * 8 / NT;  // 16-byte X chunks per thread per stage (= MF)
@@ -115,10 +120,23 @@ __global__ void __launch_bounds__(256 * WM, 2 / WM) k_gemm(GemmArgs a) {
   uint16_t* lds0 = smem;
   uint16_t* lds1 = smem + BM * kBK;
 
-  const int split = blockIdx.x % a.splits;
-  const int tile = blockIdx.x / a.splits;
-  const int row0 = blockIdx.y * BM;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // Workgroup id -> (column tile, split, row block). The row blocks of one
+  // (tile, split) sit 8 ids apart: dispatch deals ids round-robin to the 8
+  // XCDs, so they run together on one XCD and share its L2 for the weights.
+  int pair, mblk;
+  {
+    const int L = blockIdx.x;
+    const int per_group = 8 * a.mblocks;
+    const int r = L % per_group;
+    pair = (L / per_group) * 8 + (r % 8);
+    mblk = r / 8;
+    if (pair >= a.tiles * a.splits) return;
+  }
+  const int split = pair % a.splits;
+  const int tile = pair / a.splits;
+  const int row0 = mblk * BM;
+  // wave index made provably uniform so weight offsets live in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave >> 2, wn = wave & 3;
   const int ng = tile * kWaves + wn;
   const bool active = ng < a.NG;
@@ -149,8 +167,12 @@ __global__ void __launch_bounds__(256 * WM, 2 / WM) k_gemm(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; r++) acc[m][n][r] = 0.f;
 
+  const int arow = wm * MF * 32 + (lane & 31);
   u32x4_t xs[CPT];
-  u32x4_t wcur[8], wnxt[8];
+  // Weight fragments of a k-tile in two halves (k steps 0-1 and 2-3). The
+  // next tile's low half is fetched at the top of an iteration, its high half
+  // once the current low half is consumed, so 48 registers hold weights.
+  u32x4_t wlo[4], whi[4], nlo[4], nhi[4];
 
   auto load_x = [&](int kt) {
 #pragma unroll
@@ -165,49 +187,61 @@ __global__ void __launch_bounds__(256 * WM, 2 / WM) k_gemm(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < CPT; i++) {
       const int r = x_row[i];
-      *(u32x4_t*)(lds + r * kBK + ((x_cc[i] ^ (r & 7)) << 3)) = xs[i];
+      *(u32x4_t*)(lds + r * kBK + ((x_cc[i] ^ ((r >> 1) & 7)) << 3)) = xs[i];
     }
   };
-  auto load_w = [&](int kt, u32x4_t (&w)[8]) {
-    const uint32_t soff = w_base + (uint32_t)kt * 8192u;
+  // fragments (kb, nf) of tile kt live at 1 KB * (kb * 2 + nf) in the tile's 8 KB
+  auto load_w_half = [&](int kt, int half, u32x4_t (&w)[4]) {
+    const uint32_t soff = w_base + (uint32_t)kt * 8192u + (uint32_t)half * 4096u;
 #pragma unroll
-    for (int j = 0; j < 8; j++) w[j] = buf_load16(wr_rsrc, w_lane + j * 1024u, soff);
+    for (int j = 0; j < 4; j++) w[j] = buf_load16(wr_rsrc, w_lane + j * 1024u, soff);
+  };
+  auto mma_half = [&](const uint16_t* cur, int half, const u32x4_t (&w)[4]) {
+#pragma unroll
+    for (int kh = 0; kh < 2; kh++) {
+      const int kb = half * 2 + kh;
+      const int cc = kb * 2 + (lane >> 5);
+#pragma unroll
+      for (int m = 0; m < MF; m++) {
+        const int r = arow + m * 32;
+        const bf16x8_t af = as_bf16x8(*(const u32x4_t*)(cur + r * kBK + ((cc ^ ((r >> 1) & 7)) << 3)));
+        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(w[kh * 2 + 0]), acc[m][0], 0, 0, 0);
+        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(w[kh * 2 + 1]), acc[m][1], 0, 0, 0);
+      }
+    }
   };
 
   if (kt0 < kt1) {
     load_x(kt0);
-    if (active) load_w(kt0, wcur);
+    if (active) {
+      load_w_half(kt0, 0, wlo);
+      load_w_half(kt0, 1, whi);
+    }
     store_x(lds0);
   }
   __syncthreads();
 
-  const int arow = wm * MF * 32 + (lane & 31);
   for (int kt = kt0; kt < kt1; kt++) {
     const uint16_t* cur = ((kt - kt0) & 1) ? lds1 : lds0;
     uint16_t* nxt = ((kt - kt0) & 1) ? lds0 : lds1;
     const bool more = kt + 1 < kt1;
     if (more) {
       load_x(kt + 1);
-      if (active) load_w(kt + 1, wnxt);
+      if (active) load_w_half(kt + 1, 0, nlo);
     }
     if (active) {
-#pragma unroll
-      for (int kb = 0; kb < 4; kb++) {
-        const int cc = kb * 2 + (lane >> 5);
-#pragma unroll
-        for (int m = 0; m < MF; m++) {
-          const int r = arow + m * 32;
-          const bf16x8_t af = as_bf16x8(*(const u32x4_t*)(cur + r * kBK + ((cc ^ (r & 7)) << 3)));
-          acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(wcur[kb * 2 + 0]), acc[m][0], 0, 0, 0);
-          acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(wcur[kb * 2 + 1]), acc[m][1], 0, 0, 0);
-        }
-      }
+      mma_half(cur, 0, wlo);
+      if (more) load_w_half(kt + 1, 1, nhi);
+      mma_half(cur, 1, whi);
     }
     if (more) store_x(nxt);
     __syncthreads();
     if (more) {
 #pragma unroll
-      for (int j = 0; j < 8; j++) wcur[j] = wnxt[j];
+      for (int j = 0; j < 4; j++) {
+        wlo[j] = nlo[j];
+        whi[j] = nhi[j];
+      }
     }
   }
 
@@ -283,12 +317,11 @@ size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k,
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int NG = round_up(n_cols_packed, 64) / 64;
   const int tiles = (NG + kWaves - 1) / kWaves;
-  const int mblocks = (M + 255) / 256;
+  const int mblocks = (M + 127) / 128;
   const int KT = round_up(K, 64) / kBK;
   const int base = tiles * mblocks;
-  // Workgroups of up to 128 rows are 4 waves and two fit per CU; 256-row
-  // workgroups are 8 waves, one per CU.
-  const int target = M <= 128 ? 2 * num_cus : num_cus;
+  // 4-wave workgroups of up to 128 rows; two fit per CU.
+  const int target = 2 * num_cus;
   int s = (target + base / 2) / base;
   if (s < 1) s = 1;
   if (s > 16) s = 16;
@@ -319,7 +352,9 @@ hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, voi
 }
 
 template <int MF, int WM, int EPI, bool P>
-static hipError_t launch_mf(const GemmArgs& a, int mblocks, hipStream_t s) {
+static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
+  constexpr int BM = WM * MF * 32;
+  a.mblocks = (a.M + BM - 1) / BM;
   const size_t lds = (size_t)2 * WM * MF * 32 * kBK * sizeof(uint16_t);
   static bool attr_set = false;
   if (!attr_set) {
@@ -328,19 +363,27 @@ static hipError_t launch_mf(const GemmArgs& a, int mblocks, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  dim3 grid(a.tiles * a.splits, mblocks);
+  const int pairs = a.tiles * a.splits;
+  const int grid = (pairs + 7) / 8 * 8 * a.mblocks;
   k_gemm<MF, WM, EPI, P><<<grid, 256 * WM, lds, s>>>(a);
   return hipGetLastError();
 }
 
+static int gemm_variant() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = std::getenv("SIDP_GEMM_VARIANT");
+    v = e ? std::atoi(e) : 0;
+  }
+  return v;
+}
+
 template <int EPI, bool P>
 static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  const int mblocks = (a.M + 255) / 256;
-  const int mrows = a.M <= 256 ? a.M : 256;
-  if (mrows <= 32) return launch_mf<1, 1, EPI, P>(a, mblocks, s);
-  if (mrows <= 64) return launch_mf<2, 1, EPI, P>(a, mblocks, s);
-  if (mrows <= 128) return launch_mf<4, 1, EPI, P>(a, mblocks, s);
-  return launch_mf<4, 2, EPI, P>(a, mblocks, s);
+  if (a.M <= 32) return launch_mf<1, 1, EPI, P>(a, s);
+  if (a.M <= 64) return launch_mf<2, 1, EPI, P>(a, s);
+  if (a.M <= 128 || gemm_variant() == 0) return launch_mf<4, 1, EPI, P>(a, s);
+  return launch_mf<4, 2, EPI, P>(a, s);
 }
 
 hipError_t launch_linear(const LinearCall& c, hipStream_t s) {

@@ -474,6 +474,7 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   a.part = h->attn_part;
   a.max_parts = h->attn_max_parts;
   a.err = h->err;
+  a.num_cus = h->num_cus;
   TIMED(h, SIDP_K_ATTN, s, launch_attention(a, s));
   // a7: O projection + residual (in place on the fp32 residual stream)
   TIMED(h, SIDP_K_O, s,
@@ -503,7 +504,8 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, int flags, hip
     if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst, src, lb, hipMemcpyDeviceToDevice, cp);
-  else e = launch_copy(src, dst, lb, h->copy_grid, cp);
+  else if (flags & SIDP_COPY_BURST) e = launch_copy(src, dst, lb, h->copy_grid, cp);
+  else e = launch_fill_bg(src, dst, lb, h->num_cus, cp);
   if (e != hipSuccess) return e;
   if ((e = time_end(h, cp)) != hipSuccess) return e;
   return hipEventRecord(h->filled[slot], cp);
@@ -726,6 +728,7 @@ int sidp_attention(sidp_handle* h, const void* q, int32_t region, const int32_t*
   a.part = h->attn_part;
   a.max_parts = h->attn_max_parts;
   a.err = h->err;
+  a.num_cus = h->num_cus;
   HIPCHK(h, launch_attention(a, (hipStream_t)stream));
   h->last_compute = (hipStream_t)stream;
   return SIDP_OK;
