@@ -201,14 +201,21 @@ int sidp_sync(sidp_handle *h);
 int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
 
 /* ---- the slot-ring plan (host only) ----
- * The order in which sidp_decode_step issues ring operations for `steps`
- * streamed calls of num_layers layers, 2 slots. Each op is 3 int32
- * {kind, global layer g, slot}; kinds: 0 fill, 1 wait-fill, 2 compute,
- * 3 done, 4 wait-done. copy_ops/compute_ops receive up to *n_copy/*n_compute
- * ops (host arrays of 3*capacity int32); on return the counts are the numbers
- * of ops written. SIDP_EINVAL if a capacity is too small. */
-int sidp_plan(int32_t num_layers, int32_t steps, int32_t *copy_ops, int32_t *n_copy,
-              int32_t *compute_ops, int32_t *n_compute);
+ * The order in which sidp_decode_step issues its ring operations on the two
+ * streams, for `steps` streamed calls of num_layers layers with 2 slots. Layer
+ * g (counted across calls) computes from slot g % 2 while layer g + 1 is
+ * copied into the other slot as two tiles (§4.2 "tensor tiles", each with its
+ * notification): tile A once layer g - 1 has released the slot, tile B once
+ * layer g's attention half has been issued, so that it runs beside layer g's
+ * projections. Each op is 3 int32 {kind, layer g, slot}; kinds:
+ *   0 copy tile A of layer g          1 copy tile B of layer g, then mark filled
+ *   2 compute waits for the fill      3 attention half of layer g
+ *   4 mark attention half issued      5 projection half of layer g
+ *   6 mark slot released              7 copy stream waits for the release
+ *   8 copy stream waits for the attention half.
+ * ops (host, 3 * *n_ops int32) receives up to *n_ops ops; on return *n_ops is
+ * the number written. SIDP_EINVAL if the capacity is too small. */
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t *ops, int32_t *n_ops);
 
 /* ---- single kernels, for parity checks and reuse ----
  * All enqueue on `stream` and return immediately. */

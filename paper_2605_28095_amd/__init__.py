@@ -37,7 +37,8 @@ SIDP_EPI_BF16 = 0
 SIDP_EPI_RESID = 1
 SIDP_EPI_SWIGLU = 2
 
-PLAN_OPS = {0: "fill", 1: "wait_fill", 2: "compute", 3: "done", 4: "wait_done"}
+PLAN_OPS = {0: "fill_a", 1: "fill_b", 2: "wait_fill", 3: "attn", 4: "mid", 5: "proj", 6: "done", 7: "wait_done",
+            8: "wait_mid"}
 
 EXPORTED = [
     "sidp_strerror", "sidp_last_hip_error", "sidp_create", "sidp_destroy", "sidp_layer_bytes",
@@ -93,7 +94,7 @@ _sigs = {
     "sidp_kv_attach": (ctypes.c_int, [_P, _P, _P, _I, _I]),
     "sidp_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _I, _P, _P]),
     "sidp_sync": (ctypes.c_int, [_P]),
-    "sidp_plan": (ctypes.c_int, [_I, _I, _PI, _PI, _PI, _PI]),
+    "sidp_plan": (ctypes.c_int, [_I, _I, _PI, _PI]),
     "sidp_rmsnorm": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I, _I, _P]),
     "sidp_packed_bytes": (_Z, [_I, _I]),
     "sidp_pack_linear": (ctypes.c_int, [_P, _I, _I, _P, _P]),
@@ -205,14 +206,12 @@ def sidp_sync(h):
 
 
 def sidp_plan(num_layers, steps):
-    """(copy_ops, compute_ops) as lists of (kind name, g, slot)."""
-    cap_c, cap_k = 2 * num_layers * steps + 2, 3 * num_layers * steps + 1
-    cbuf = (ctypes.c_int32 * (3 * cap_c))()
-    kbuf = (ctypes.c_int32 * (3 * cap_k))()
-    nc, nk = ctypes.c_int32(cap_c), ctypes.c_int32(cap_k)
-    _check(_lib.sidp_plan(num_layers, steps, cbuf, ctypes.byref(nc), kbuf, ctypes.byref(nk)), "sidp_plan")
-    conv = lambda buf, n: [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n)]  # noqa: E731
-    return conv(cbuf, nc.value), conv(kbuf, nk.value)
+    """Ring operations in issue order, as (kind name, layer g, slot)."""
+    cap = 9 * num_layers * steps + 2
+    buf = (ctypes.c_int32 * (3 * cap))()
+    n = ctypes.c_int32(cap)
+    _check(_lib.sidp_plan(num_layers, steps, buf, ctypes.byref(n)), "sidp_plan")
+    return [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n.value)]
 
 
 def sidp_rmsnorm(x, gain, eps, out, rows, n, stream=None):

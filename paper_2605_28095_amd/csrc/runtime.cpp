@@ -30,6 +30,7 @@ namespace {
 constexpr int kSlots = 2;
 constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
+constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
@@ -72,27 +73,44 @@ bool config_ok(const sidp_config* c) {
   return true;
 }
 
-// Ring operation kinds (shared with sidp_plan).
-enum { OP_FILL = 0, OP_WAIT_FILL = 1, OP_COMPUTE = 2, OP_DONE = 3, OP_WAIT_DONE = 4 };
+// Ring operations, in host issue order (shared with sidp_plan). Layer g
+// (counted across calls) computes from slot g % 2 while layer g + 1 is copied
+// into the other slot, in two parts: part A as soon as layer g - 1 has
+// released that slot, part B once layer g's attention half has been issued,
+// so that it runs beside the projections (MFMA-bound, spare HBM bandwidth).
+enum {
+  OP_FILL_A = 0,     // copy stream: first part of layer g's blob into slot
+  OP_FILL_B = 1,     // copy stream: the rest, then mark the slot filled
+  OP_WAIT_FILL = 2,  // compute stream waits for the slot's fill
+  OP_ATTN = 3,       // compute: attention half of layer g
+  OP_MID = 4,        // compute: mark layer g's attention half issued
+  OP_PROJ = 5,       // compute: projection half of layer g
+  OP_DONE = 6,       // compute: mark the slot released
+  OP_WAIT_DONE = 7,  // copy stream waits for layer g to release its slot
+  OP_WAIT_MID = 8,   // copy stream waits for layer g's attention half
+};
 struct RingOp {
   int kind;
   int64_t g;
   int slot;
 };
 
-// The static ring plan. Before the first streamed layer: fills of the first
-// kSlots layers. For layer g: compute side {wait fill g, compute g, done g};
-// copy side {wait done g, fill g + kSlots} into the slot g just released.
-void ring_prologue(int64_t g0, std::vector<RingOp>& copy_ops) {
-  for (int i = 0; i < kSlots; i++) copy_ops.push_back({OP_FILL, g0 + i, (int)((g0 + i) % kSlots)});
+void ring_prologue(int64_t g0, std::vector<RingOp>& ops) {
+  ops.push_back({OP_FILL_A, g0, (int)(g0 % kSlots)});
+  ops.push_back({OP_FILL_B, g0, (int)(g0 % kSlots)});
 }
-void ring_layer(int64_t g, std::vector<RingOp>& copy_ops, std::vector<RingOp>& compute_ops) {
-  const int s = (int)(g % kSlots);
-  compute_ops.push_back({OP_WAIT_FILL, g, s});
-  compute_ops.push_back({OP_COMPUTE, g, s});
-  compute_ops.push_back({OP_DONE, g, s});
-  copy_ops.push_back({OP_WAIT_DONE, g, s});
-  copy_ops.push_back({OP_FILL, g + kSlots, s});
+// first: g is the first streamed layer since pool_init (its neighbour slot was never used).
+void ring_layer(int64_t g, bool first, std::vector<RingOp>& ops) {
+  const int s = (int)(g % kSlots), n = (int)((g + 1) % kSlots);
+  if (!first) ops.push_back({OP_WAIT_DONE, g - 1, n});
+  ops.push_back({OP_FILL_A, g + 1, n});
+  ops.push_back({OP_WAIT_FILL, g, s});
+  ops.push_back({OP_ATTN, g, s});
+  ops.push_back({OP_MID, g, s});
+  ops.push_back({OP_WAIT_MID, g, s});
+  ops.push_back({OP_FILL_B, g + 1, n});
+  ops.push_back({OP_PROJ, g, s});
+  ops.push_back({OP_DONE, g, s});
 }
 
 }  // namespace
@@ -121,7 +139,8 @@ struct sidp_handle {
   int attn_max_parts = 0;
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
-  hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {};
+  hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
+  size_t fill_split = 0;  // bytes of a layer blob in fill part A
   bool events_ok = false;
   // ring state
   bool ring_started = false;
@@ -177,6 +196,7 @@ static void free_device(sidp_handle* h) {
   for (int i = 0; i < kSlots; i++) {
     if (h->filled[i]) (void)hipEventDestroy(h->filled[i]);
     if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
+    if (h->mid[i]) (void)hipEventDestroy(h->mid[i]);
   }
   for (auto& t : h->timed) {
     (void)hipEventDestroy(t.a);
@@ -250,6 +270,13 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   for (int i = 0; i < kSlots; i++) {
     if (hipEventCreateWithFlags(&h->filled[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
+    if (hipEventCreateWithFlags(&h->mid[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
+  }
+  {
+    int pct = kFillPartAPercent;
+    if (const char* e = std::getenv("SIDP_FILL_SPLIT")) pct = std::min(100, std::max(0, std::atoi(e)));
+    h->fill_split = align_up(h->blob.total * (size_t)pct / 100, kAlign);
+    if (h->fill_split > h->blob.total) h->fill_split = h->blob.total;
   }
   *out = h;
   return SIDP_OK;
@@ -425,12 +452,13 @@ static hipError_t time_end(sidp_handle* h, hipStream_t s) {
     if ((te_ = time_end((h), (s))) != hipSuccess) return te_;       \
   } while (0)
 
-// The per-layer kernel sequence, reading weights from `wb` (a pool blob or a slot).
-static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, const int32_t* positions,
-                            const int32_t* bt, int max_blocks, int B, hipStream_t s) {
+// The attention half of a layer (norm, QKV, QK-norm/RoPE/KV append,
+// attention), reading weights from `wb` (a pool blob or a slot).
+static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, const int32_t* positions,
+                                const int32_t* bt, int max_blocks, int B, hipStream_t s) {
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
-  const int H = c.hidden, D = c.head_dim, QD = c.num_q_heads * D;
+  const int H = c.hidden, D = c.head_dim;
   // a2: RMSNorm before attention
   TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
   // a3: QKV projection (+ bias)
@@ -476,6 +504,15 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   a.err = h->err;
   a.num_cus = h->num_cus;
   TIMED(h, SIDP_K_ATTN, s, launch_attention(a, s));
+  return hipSuccess;
+}
+
+// The projection half of a layer (O + residual, norm, gate/up + SwiGLU,
+// down + residual).
+static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, float* hidden, int B, hipStream_t s) {
+  const sidp_config& c = h->cfg;
+  const BlobLayout& L = h->blob;
+  const int H = c.hidden, QD = c.num_q_heads * c.head_dim;
   // a7: O projection + residual (in place on the fp32 residual stream)
   TIMED(h, SIDP_K_O, s,
         launch_linear(linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s));
@@ -492,23 +529,31 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   return hipSuccess;
 }
 
-// One slot fill on the copy stream: layer (g mod L) from the pool into `slot`.
-static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, int flags, hipStream_t cp) {
+static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, const int32_t* positions,
+                            const int32_t* bt, int max_blocks, int B, hipStream_t s) {
+  hipError_t e = run_attn_half(h, wb, layer, hidden, positions, bt, max_blocks, B, s);
+  if (e != hipSuccess) return e;
+  return run_proj_half(h, wb, hidden, B, s);
+}
+
+// Part of one slot fill on the copy stream: bytes [lo, hi) of layer (g mod L)
+// from the pool into `slot`. The debug poison and delay precede the first part.
+static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, size_t hi, int flags, hipStream_t cp) {
   const size_t lb = h->blob.total;
   uint8_t* dst = h->slots + (size_t)slot * lb;
   const uint8_t* src = h->pool + (size_t)(g % h->cfg.num_layers) * lb;
   hipError_t e;
-  if (flags & SIDP_DEBUG_POISON)
+  if (lo == 0 && (flags & SIDP_DEBUG_POISON))
     if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
-  if (flags & SIDP_DEBUG_DELAY)
+  if (lo == 0 && (flags & SIDP_DEBUG_DELAY))
     if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
+  if (hi <= lo) return hipSuccess;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
-  if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst, src, lb, hipMemcpyDeviceToDevice, cp);
-  else if (flags & SIDP_COPY_BURST) e = launch_copy(src, dst, lb, h->copy_grid, cp);
-  else e = launch_fill_bg(src, dst, lb, h->num_cus, cp);
+  if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
+  else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
+  else e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, cp);
   if (e != hipSuccess) return e;
-  if ((e = time_end(h, cp)) != hipSuccess) return e;
-  return hipEventRecord(h->filled[slot], cp);
+  return time_end(h, cp);
 }
 
 int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, const int32_t* block_tables,
@@ -538,34 +583,54 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
 
   h->last_copy = cp;
   h->any_copy = true;
-  std::vector<RingOp> copy_ops, compute_ops;
+  std::vector<RingOp> ops;
+  bool first = false;
   if (!h->ring_started) {
-    ring_prologue(h->ring_g, copy_ops);
+    ring_prologue(h->ring_g, ops);
     h->ring_started = true;
+    first = true;
   }
-  for (RingOp& op : copy_ops) HIPCHK(h, issue_fill(h, op.g, op.slot, flags, cp));
-  copy_ops.clear();
   for (int l = 0; l < c.num_layers; l++) {
     const int64_t g = h->ring_g++;
-    ring_layer(g, copy_ops, compute_ops);
-    for (RingOp& op : compute_ops) {
-      if (op.kind == OP_WAIT_FILL) {
+    ring_layer(g, first && l == 0, ops);
+  }
+  const size_t lb = h->blob.total;
+  for (const RingOp& op : ops) {
+    const uint8_t* slot = h->slots + (size_t)op.slot * lb;
+    switch (op.kind) {
+      case OP_FILL_A:
+        HIPCHK(h, issue_fill(h, op.g, op.slot, 0, h->fill_split, flags, cp));
+        break;
+      case OP_FILL_B:
+        HIPCHK(h, issue_fill(h, op.g, op.slot, h->fill_split, lb, flags, cp));
+        HIPCHK(h, hipEventRecord(h->filled[op.slot], cp));
+        break;
+      case OP_WAIT_FILL:
         // under SIDP_TIMING the interval around the wait is the compute stall on the fill
         HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
         HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
         HIPCHK(h, time_end(h, cs));
-      }
-      else if (op.kind == OP_COMPUTE)
-        HIPCHK(h, run_layer(h, h->slots + (size_t)op.slot * h->blob.total, (int)(op.g % c.num_layers), hidden,
-                            positions, block_tables, max_blocks_per_seq, batch, cs));
-      else if (op.kind == OP_DONE) HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
+        break;
+      case OP_ATTN:
+        HIPCHK(h, run_attn_half(h, slot, (int)(op.g % c.num_layers), hidden, positions, block_tables,
+                                max_blocks_per_seq, batch, cs));
+        break;
+      case OP_MID:
+        HIPCHK(h, hipEventRecord(h->mid[op.slot], cs));
+        break;
+      case OP_PROJ:
+        HIPCHK(h, run_proj_half(h, slot, hidden, batch, cs));
+        break;
+      case OP_DONE:
+        HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
+        break;
+      case OP_WAIT_DONE:
+        HIPCHK(h, hipStreamWaitEvent(cp, h->consumed[op.slot], 0));
+        break;
+      case OP_WAIT_MID:
+        HIPCHK(h, hipStreamWaitEvent(cp, h->mid[op.slot], 0));
+        break;
     }
-    for (RingOp& op : copy_ops) {
-      if (op.kind == OP_WAIT_DONE) HIPCHK(h, hipStreamWaitEvent(cp, h->consumed[op.slot], 0));
-      else if (op.kind == OP_FILL) HIPCHK(h, issue_fill(h, op.g, op.slot, flags, cp));
-    }
-    copy_ops.clear();
-    compute_ops.clear();
   }
   return SIDP_OK;
 }
@@ -605,26 +670,19 @@ int sidp_timing_collect(sidp_handle* h, double* ms, int32_t* launches) {
   return SIDP_OK;
 }
 
-int sidp_plan(int32_t num_layers, int32_t steps, int32_t* copy_ops, int32_t* n_copy, int32_t* compute_ops,
-              int32_t* n_compute) {
-  if (num_layers < 1 || steps < 0 || !n_copy || !n_compute) return SIDP_EINVAL;
-  std::vector<RingOp> cp, co;
-  if (steps > 0) ring_prologue(0, cp);
-  for (int64_t g = 0; g < (int64_t)num_layers * steps; g++) ring_layer(g, cp, co);
-  if ((int64_t)cp.size() > *n_copy || (int64_t)co.size() > *n_compute) return SIDP_EINVAL;
-  if ((!cp.empty() && !copy_ops) || (!co.empty() && !compute_ops)) return SIDP_EINVAL;
-  for (size_t i = 0; i < cp.size(); i++) {
-    copy_ops[3 * i] = cp[i].kind;
-    copy_ops[3 * i + 1] = (int32_t)cp[i].g;
-    copy_ops[3 * i + 2] = cp[i].slot;
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t* ops_out, int32_t* n_ops) {
+  if (num_layers < 1 || steps < 0 || !n_ops) return SIDP_EINVAL;
+  std::vector<RingOp> ops;
+  if (steps > 0) ring_prologue(0, ops);
+  for (int64_t g = 0; g < (int64_t)num_layers * steps; g++) ring_layer(g, g == 0, ops);
+  if ((int64_t)ops.size() > *n_ops) return SIDP_EINVAL;
+  if (!ops.empty() && !ops_out) return SIDP_EINVAL;
+  for (size_t i = 0; i < ops.size(); i++) {
+    ops_out[3 * i] = ops[i].kind;
+    ops_out[3 * i + 1] = (int32_t)ops[i].g;
+    ops_out[3 * i + 2] = ops[i].slot;
   }
-  for (size_t i = 0; i < co.size(); i++) {
-    compute_ops[3 * i] = co[i].kind;
-    compute_ops[3 * i + 1] = (int32_t)co[i].g;
-    compute_ops[3 * i + 2] = co[i].slot;
-  }
-  *n_copy = (int32_t)cp.size();
-  *n_compute = (int32_t)co.size();
+  *n_ops = (int32_t)ops.size();
   return SIDP_OK;
 }
 

@@ -217,20 +217,34 @@ def test_slot_mapping_brute_force():
 # ---------------------------------------------------------------- schedule
 
 def test_was_schedule_ordering():
-    L, steps, n = 5, 3, 2
-    copy_ops, comp_ops = was_schedule(L, steps, n)
+    """Properties the paper's buffer management requires, checked on the
+    issue order: every layer is fully read into its slot before compute on it
+    starts, a slot is refilled only after its previous layer released it, at
+    most two layers occupy the cache, and the lookahead is one layer."""
+    L, steps = 5, 3
+    ops = was_schedule(L, steps)
     total = L * steps
-    fills = [g for (op, g, s) in copy_ops if op == "fill"]
-    assert fills == list(range(total + n))  # always n layers ahead
-    for (op, g, s) in copy_ops + comp_ops:
-        assert s == g % n
-    # compute g waits its own fill; fill g+n waits compute g's done
-    assert [g for (op, g, s) in comp_ops if op == "wait_fill"] == list(range(total))
-    for i, (op, g, s) in enumerate(copy_ops):
-        if op == "fill" and g >= n:
-            assert copy_ops[i - 1] == ("wait_done", g - n, s)
-    # at most n layers resident: between wait_done(g) and fill(g+n) no other fill to s
-    assert was_schedule(L, 0, n) == ([], [])
+    pos = {op: i for i, op in enumerate(ops)}
+    assert len(pos) == len(ops)  # no duplicates
+    for g in range(total):
+        s = g % 2
+        # compute on layer g: wait for its fill, then both halves, then release
+        seq = [pos[(k, g, s)] for k in ("wait_fill", "attn", "mid", "proj", "done")]
+        assert seq == sorted(seq)
+        # both tiles of layer g were issued before the wait on them
+        assert pos[("fill_a", g, s)] < pos[("fill_b", g, s)] < pos[("wait_fill", g, s)]
+        if g >= 1:
+            # tile A of layer g + 1 waits for layer g - 1 (same slot) to be released
+            assert pos[("done", g - 1, (g + 1) % 2)] < pos[("wait_done", g - 1, (g + 1) % 2)]
+            assert pos[("wait_done", g - 1, (g + 1) % 2)] < pos[("fill_a", g + 1, (g + 1) % 2)]
+        # tile B of layer g + 1 follows layer g's attention half
+        assert pos[("mid", g, s)] < pos[("wait_mid", g, s)] < pos[("fill_b", g + 1, (g + 1) % 2)]
+        # lookahead of one layer: layer g + 2 is not read before layer g is released
+        if ("fill_a", g + 2, s) in pos:
+            assert pos[("done", g, s)] < pos[("fill_a", g + 2, s)]
+    # fills are issued for every layer, plus one ahead into the next iteration
+    assert [g for (k, g, s) in ops if k == "fill_a"] == list(range(total + 1))
+    assert was_schedule(L, 0) == []
 
 
 # ---------------------------------------------------------------- whole layer
