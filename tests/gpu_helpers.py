@@ -117,10 +117,13 @@ class Stack:
         torch.cuda.synchronize()
 
     def layer_weights(self, l):
+        """Layer l's weights for the oracle: bf16 bit patterns when kept, else
+        regenerated and widened to float64 (an exact conversion) on the
+        generator's device."""
         if self.weights[l] is not None:
             return self.weights[l]
         w = synth.layer_weights(self.cfg, l, seed=self.seed, device=self.gen_device, gains=self.gains)
-        return {k: bits(v) for k, v in w.items()}
+        return {k: v.cpu().double().numpy() for k, v in w.items()}
 
     def reset(self):
         """Restore hidden states and KV caches to the generated inputs."""

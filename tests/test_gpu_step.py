@@ -11,7 +11,10 @@ evaluation: one element rounded the other way (fp32 vs float64 arithmetic
 near a rounding boundary) perturbs the next layers' inputs and flips further
 roundings, so two valid bf16 evaluations drift apart about as far as the
 bf16-rounding oracle drifts from the exact one (about 1e-2 after 8
-layers of the 72B shape).
+layers of the 72B shape). On the 80-layer 70B-shaped stack that drift of the
+oracle's own two evaluations reaches 2.8-3.3e-2 per row (measured), past the
+2e-2 bar: there the full-depth check uses 2x that drift, 6.5e-2, and the 2e-2
+bar is checked on the first 10 layers of the same full-size configuration.
 """
 
 import numpy as np
@@ -221,5 +224,49 @@ def test_qwen25_stack8_streamed_sampled_rows(lib):
         want, _, _, _ = st.run_oracle(rows)
         want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
         _check_hidden(got, want, want_exact, "8-layer 72B-shaped stack", tight=False)
+    finally:
+        st.close()
+
+
+def _stack80(layers, regions=4):
+    cfg = synth.get_config("llama70b_stack80", num_layers=layers)
+    return Stack(cfg, keep_weights=False, regions=regions)
+
+
+def test_llama70b_stack80_first10_layers_parity(lib):
+    """The benchmark's launch configuration (B=256, contexts up to 8K, 16-token
+    paged KV, streamed through the 2-slot ring) for 10 of its layers."""
+    st = _stack80(10)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        rows = [0, 255]
+        got = st.hidden.double().cpu().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
+        _check_hidden(got, want, want_exact, "70B shape, 10 layers", tight=False)
+    finally:
+        st.close()
+
+
+@pytest.mark.slow
+def test_llama70b_stack80_full_depth(lib):
+    """All 80 layers at B=256: streamed and resident weights give identical
+    bits; sampled rows stay within 2x the drift between the oracle's own bf16
+    and exact evaluations at this depth."""
+    st = _stack80(80)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        streamed = st.hidden.cpu().clone()
+        st.reset()
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
+        st.dec.sync()
+        assert torch.equal(st.hidden.cpu(), streamed)
+        rows = [255]
+        got = streamed.double().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        e = row_rel_err(got, want)
+        assert np.all(np.isfinite(got)) and e.max() <= 6.5e-2, e
     finally:
         st.close()
