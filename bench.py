@@ -65,6 +65,32 @@ def algorithmic_work(cfg, B, seq_total, layer_bytes):
     return w
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None if there is none or the kernel's sources changed since."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*_traffic.md")):
+        text = open(path).read()
+        start = text.rfind("```json")
+        if start < 0:
+            continue
+        try:
+            rec = json.loads(text[start + 7:text.index("```", start + 7)])
+        except ValueError:
+            continue
+        if rec.get("kernel") != kernel:
+            continue
+        h = hashlib.sha256()
+        try:
+            for src in rec["sources"]:
+                h.update(open(os.path.join(ROOT, src), "rb").read())
+        except OSError:
+            return None
+        return rec["traffic_bytes_per_launch"] if h.hexdigest() == rec["source_sha256"] else None
+    return None
+
+
 def cpu_baseline(cfg, weights_for_layer, kv_rows, x_rows, pos_rows, tabs_rows, n_layers_sample):
     """Times the oracle (as it stands) on a bounded sample: n_layers_sample
     layers for the sampled rows; returns tokens/s extrapolated to the full
@@ -234,8 +260,9 @@ def main():
     compute_classes = [k for k in kernels if k not in ("fill", "wait_fill")]
     dom = max(compute_classes, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
+    traffic = measured_traffic(dom) if args.workload == "llama70b_stack80" and B == 256 else None
     roofline = {"kernel": dom, "bound": "hbm", "achieved": dk["GB_per_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": dk["hbm_frac"], "traffic": None,
+                "frac": dk["hbm_frac"], "traffic": traffic,
                 "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
 
     resident_ms = None
