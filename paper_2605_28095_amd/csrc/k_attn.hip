@@ -38,29 +38,50 @@ struct Chunk {
   u32x2_t v[D / 16][2];  // V^T fragments: dim 16jd + lane&15, tokens (lane>>4)*4..+3
 };
 
+// Block tables and positions are read through the scalar cache: the reads are
+// uniform per wave and nothing writes those arrays during the kernel, and
+// scalar loads are counted apart from the vector loads of the KV stream. (A
+// vector load of a block index would have to complete before the next
+// chunk's addresses exist, and vector loads complete in order, so every such
+// read would drain the chunk already in flight.)
+typedef const __attribute__((address_space(4))) int32_t cint32_t;
+
+// A chunk's source: one KV head of one sequence, tokens t0 .. t0 + 31.
+struct ChunkSrc {
+  cint32_t* bt;
+  int seq, g, t0;
+};
+
+// Loads the 24 fragments of a chunk. Every call issues the same loads, so the
+// compiler's wait before a chunk's compute counts exactly the other buffer's
+// loads. A block's base address is uniform (scalar registers); each lane adds
+// a fixed 32-bit byte offset, k_lane or v_lane, so no 64-bit per-lane address
+// is rebuilt per chunk. An out-of-range block index is replaced by block 0
+// and flagged.
 template <int D>
-__device__ __forceinline__ void load_chunk(const AttnCall& a, const int32_t* bt, int64_t region_blk, int g, int t0,
-                                           int seq, int lane, Chunk<D>& c) {
+__device__ __forceinline__ void load_chunk(const AttnCall& a, const ChunkSrc& src, int64_t region_blk,
+                                           uint32_t k_lane, uint32_t v_lane, bool& bad, Chunk<D>& c) {
   constexpr int KK = D / 32, JD = D / 16;
-  const int head = lane & 15, lg = lane >> 4;
+  constexpr int64_t kBlockBytes = 16 * D * 2;  // one KV head of one 16-token block, K or V
   int blk[2];
-  blk[0] = bt[t0 >> 4];
-  blk[1] = (t0 + 16 < seq) ? bt[(t0 >> 4) + 1] : blk[0];
+  blk[0] = src.bt[src.t0 >> 4];
+  blk[1] = (src.t0 + 16 < src.seq) ? src.bt[(src.t0 >> 4) + 1] : blk[0];
 #pragma unroll
   for (int j = 0; j < 2; j++) {
     if (blk[j] < 0 || blk[j] >= a.kv.nblk) {
-      if (lane == 0) atomicOr(a.err, SIDP_DEVERR_BLOCK);
+      bad = true;
       blk[j] = 0;
     }
   }
 #pragma unroll
   for (int j = 0; j < 2; j++) {
-    const uint16_t* kp = a.kv.k + (((region_blk + blk[j]) * a.kv.hkv + g) * 16 + head) * D + lg * 8;
+    const int64_t off = ((region_blk + blk[j]) * a.kv.hkv + src.g) * kBlockBytes;
+    const char* kb = (const char*)a.kv.k + off;
+    const char* vb = (const char*)a.kv.v + off;
 #pragma unroll
-    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = *(const u32x4_t*)(kp + kk * 32);
-    const uint16_t* vp = a.kv.v + ((region_blk + blk[j]) * a.kv.hkv + g) * (int64_t)D * 16 + lg * 4;
+    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = *(const u32x4_t*)(kb + k_lane + kk * 64);
 #pragma unroll
-    for (int jd = 0; jd < JD; jd++) c.v[jd][j] = *(const u32x2_t*)(vp + (jd * 16 + head) * 16);
+    for (int jd = 0; jd < JD; jd++) c.v[jd][j] = *(const u32x2_t*)(vb + v_lane + jd * 512);
   }
 }
 
@@ -142,7 +163,7 @@ __device__ __forceinline__ int seq_parts(const AttnCall& a, int b) {
 // Items of sequence b are prefix[b] * Hkv .. prefix[b+1] * Hkv - 1, ordered
 // (partition, KV head); prefix[] is built in LDS once per workgroup.
 template <int D>
-__global__ void __launch_bounds__(256, 2) k_attn(AttnCall a) {
+__global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) k_attn(AttnCall a) {
   constexpr int KK = D / 32, JD = D / 16;
   extern __shared__ __attribute__((aligned(16))) float smem_f[];
   float* s_m = smem_f;                             // [4][16]
@@ -190,84 +211,133 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnCall a) {
   const int total_items = s_prefix[B] * a.hkv;
   const float scale = kLog2e / sqrtf((float)D);
   const int64_t region_blk = (int64_t)a.region * a.kv.nblk;
+  cint32_t* positions = (cint32_t*)a.positions;
 
-  for (int item = blockIdx.x; item < total_items; item += gridDim.x) {
-    const int pg = item / a.hkv, g = item % a.hkv;
+  // An item's parameters; all uniform. This wave's tokens are [tb, te).
+  struct Item {
+    int b, part, nparts, seq, g, tb, te;
+    cint32_t* bt;
+  };
+  auto get_item = [&](int item, Item& it) {
+    const int pg = item / a.hkv;
+    it.g = item % a.hkv;
     int lo_b = 0, hi_b = B - 1;  // last b with prefix[b] <= pg
     while (lo_b < hi_b) {
       const int mid = (lo_b + hi_b + 1) >> 1;
       if (s_prefix[mid] <= pg) lo_b = mid;
       else hi_b = mid - 1;
     }
-    const int b = lo_b;
-    const int part = pg - s_prefix[b];
-    const int nparts = s_prefix[b + 1] - s_prefix[b];
-    const int seq = a.positions[b] + 1;
-    const int32_t* bt = a.block_tables + (int64_t)b * a.max_blocks;
+    it.b = __builtin_amdgcn_readfirstlane(lo_b);
+    it.part = pg - s_prefix[it.b];
+    it.nparts = s_prefix[it.b + 1] - s_prefix[it.b];
+    it.seq = positions[it.b] + 1;
+    it.bt = (cint32_t*)(a.block_tables + (int64_t)it.b * a.max_blocks);
+    it.tb = it.part * kPartTokens + wave * kWaveTokens;
+    it.te = min(it.tb + kWaveTokens, it.seq);
+  };
+  // Query heads ride in the 16 MFMA columns; lanes past the group load a
+  // duplicate of the group's first head (finite values whose columns are never
+  // merged or written), so the loaded fragments feed the MFMA unmodified and
+  // no wait is needed until the first chunk's compute.
+  auto load_q = [&](const Item& it, bf16x8_t (&q)[KK]) {
+    const int qh = it.g * group + (head < group ? head : 0);
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++)
+      q[kk] = as_bf16x8(*(const u32x4_t*)(a.q + ((int64_t)it.b * a.hq + qh) * D + lg * 8 + kk * 32));
+  };
 
+  // K fragment: token lane & 15, dims (lane >> 4) * 8 + 32 kk; V^T fragment:
+  // dim 16 jd + (lane & 15), tokens (lane >> 4) * 4 .. + 3 (byte offsets)
+  const uint32_t k_lane = (uint32_t)(head * D + lg * 8) * 2u;
+  const uint32_t v_lane = (uint32_t)(head * 16 + lg * 4) * 2u;
+  bool bad = false;
+  int item = blockIdx.x;
+  if (item < total_items) {
+    // The chunk stream of a wave runs across its items: the load slot after an
+    // item's last chunk fetches the first chunk of the wave's part of the next
+    // item (or, if there is none, re-reads the last chunk: an L2 hit that keeps
+    // every iteration's loads identical), so that load is in flight while the
+    // item's partial results are merged and written.
+    Item cur;
+    get_item(item, cur);
     bf16x8_t qb[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; kk++) {
-      u32x4_t v = {0u, 0u, 0u, 0u};
-      if (head < group) v = *(const u32x4_t*)(a.q + ((int64_t)b * a.hq + g * group + head) * D + lg * 8 + kk * 32);
-      qb[kk] = as_bf16x8(v);
-    }
-    const int t_begin = part * kPartTokens + wave * kWaveTokens;
-    const int t_end = min(t_begin + kWaveTokens, seq);
-    float m_run = -INFINITY, l_run = 0.f;
-    f32x4_t o[JD];
-#pragma unroll
-    for (int j = 0; j < JD; j++) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    // chunks of 32 tokens, two register buffers: load the next while computing one
+    load_q(cur, qb);
     Chunk<D> ca, cb;
-    if (t_begin < t_end) load_chunk<D>(a, bt, region_blk, g, t_begin, seq, lane, ca);
-    for (int t0 = t_begin; t0 < t_end; t0 += 64) {
-      const int t1 = t0 + 32;
-      if (t1 < t_end) load_chunk<D>(a, bt, region_blk, g, t1, seq, lane, cb);
-      compute_chunk<D>(ca, qb, t0, seq, lane, scale, m_run, l_run, o);
-      if (t1 + 32 < t_end) load_chunk<D>(a, bt, region_blk, g, t1 + 32, seq, lane, ca);
-      if (t1 < t_end) compute_chunk<D>(cb, qb, t1, seq, lane, scale, m_run, l_run, o);
-    }
-    l_run += __shfl_xor(l_run, 16, 64);
-    l_run += __shfl_xor(l_run, 32, 64);
+    if (cur.tb < cur.te) load_chunk<D>(a, ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb}, region_blk, k_lane, v_lane, bad, ca);
+    for (;;) {
+      const int nitem = item + gridDim.x;
+      const bool has_next = nitem < total_items;
+      Item nx = cur;
+      if (has_next) get_item(nitem, nx);
+      const bool pf = has_next && nx.tb < nx.te;
+      const int n = cur.te > cur.tb ? (cur.te - cur.tb + 31) / 32 : 0;  // this wave's chunks in the item
+      // source of stream slot i of this item (slot n is the prefetch)
+      auto src_of = [&](int i) -> ChunkSrc {
+        if (i < n) return ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb + 32 * i};
+        if (pf) return ChunkSrc{nx.bt, nx.seq, nx.g, nx.tb};
+        return ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb + 32 * (n - 1)};
+      };
 
-    if (lg == 0) {
-      s_m[wave * 16 + head] = m_run;
-      s_l[wave * 16 + head] = l_run;
-    }
+      float m_run = -INFINITY, l_run = 0.f;
+      f32x4_t o[JD];
 #pragma unroll
-    for (int jd = 0; jd < JD; jd++)
-#pragma unroll
-      for (int r = 0; r < 4; r++) s_o[(wave * 16 + head) * (D + 1) + jd * 16 + lg * 4 + r] = o[jd][r];
-    __syncthreads();
-    for (int i = threadIdx.x; i < group * D; i += 256) {
-      const int hh = i / D, d = i % D;
-      float M = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
-      float L = 0.f, O = 0.f;
-#pragma unroll
-      for (int w = 0; w < 4; w++) {
-        const float mw = s_m[w * 16 + hh];
-        const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-        L += s_l[w * 16 + hh] * f;
-        O += s_o[(w * 16 + hh) * (D + 1) + d] * f;
-      }
-      const int qh = g * group + hh;
-      if (nparts == 1) {
-        a.out[((int64_t)b * a.hq + qh) * D + d] = f2bf(O / L);
-      } else {
-        float* pp = a.part + (((int64_t)b * a.hq + qh) * a.max_parts + part) * (D + 2);
-        pp[d] = O;
-        if (d == 0) {
-          pp[D] = M;
-          pp[D + 1] = L;
+      for (int j = 0; j < JD; j++) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int i = 0; i < n; i += 2) {
+        load_chunk<D>(a, src_of(i + 1), region_blk, k_lane, v_lane, bad, cb);
+        compute_chunk<D>(ca, qb, cur.tb + 32 * i, cur.seq, lane, scale, m_run, l_run, o);
+        if (i + 1 < n) {
+          load_chunk<D>(a, src_of(i + 2), region_blk, k_lane, v_lane, bad, ca);
+          compute_chunk<D>(cb, qb, cur.tb + 32 * (i + 1), cur.seq, lane, scale, m_run, l_run, o);
         }
       }
+      // an odd count left the prefetch in cb; an idle wave has not issued it yet
+      if (n == 0 && pf) load_chunk<D>(a, src_of(0), region_blk, k_lane, v_lane, bad, ca);
+      if (has_next) load_q(nx, qb);  // qb is dead until the next item's first chunk
+
+      l_run += __shfl_xor(l_run, 16, 64);
+      l_run += __shfl_xor(l_run, 32, 64);
+      if (lg == 0) {
+        s_m[wave * 16 + head] = m_run;
+        s_l[wave * 16 + head] = l_run;
+      }
+#pragma unroll
+      for (int jd = 0; jd < JD; jd++)
+#pragma unroll
+        for (int r = 0; r < 4; r++) s_o[(wave * 16 + head) * (D + 1) + jd * 16 + lg * 4 + r] = o[jd][r];
+      __syncthreads();
+      for (int i = threadIdx.x; i < group * D; i += 256) {
+        const int hh = i / D, d = i % D;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
+        float L = 0.f, O = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; w++) {
+          const float mw = s_m[w * 16 + hh];
+          const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+          L += s_l[w * 16 + hh] * f;
+          O += s_o[(w * 16 + hh) * (D + 1) + d] * f;
+        }
+        const int qh = cur.g * group + hh;
+        if (cur.nparts == 1) {
+          a.out[((int64_t)cur.b * a.hq + qh) * D + d] = f2bf(O / L);
+        } else {
+          float* pp = a.part + (((int64_t)cur.b * a.hq + qh) * a.max_parts + cur.part) * (D + 2);
+          pp[d] = O;
+          if (d == 0) {
+            pp[D] = M;
+            pp[D + 1] = L;
+          }
+        }
+      }
+      __syncthreads();  // s_m, s_l and s_o are reused by the next item
+      if (!has_next) break;
+      if ((n & 1) && pf) ca = cb;
+      cur = nx;
+      item = nitem;
     }
-    __syncthreads();  // s_m, s_l and s_o are reused by the next item
   }
+  if (bad && lane == 0) atomicOr(a.err, SIDP_DEVERR_BLOCK);
 }
 
 // Log-sum-exp merge of a sequence's partitions: one workgroup per (head, b).

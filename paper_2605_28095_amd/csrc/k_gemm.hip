@@ -211,38 +211,32 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
     }
   };
 
-  if (kt0 < kt1) {
-    load_x(kt0);
-    if (active) {
-      load_w_half(kt0, 0, wlo);
-      load_w_half(kt0, 1, whi);
-    }
-    store_x(lds0);
-  }
-  __syncthreads();
-
-  for (int kt = kt0; kt < kt1; kt++) {
-    const uint16_t* cur = ((kt - kt0) & 1) ? lds1 : lds0;
-    uint16_t* nxt = ((kt - kt0) & 1) ? lds0 : lds1;
-    const bool more = kt + 1 < kt1;
-    if (more) {
-      load_x(kt + 1);
-      if (active) load_w_half(kt + 1, 0, nlo);
-    }
-    if (active) {
-      mma_half(cur, 0, wlo);
-      if (more) load_w_half(kt + 1, 1, nhi);
-      mma_half(cur, 1, whi);
-    }
-    if (more) store_x(nxt);
+  // Every load of the k loop is issued on every path (a wait count can only
+  // be exact when all paths issue the same loads): the prefetch past the
+  // split's last k-tile re-reads that tile (weights, an L2 hit) or reads past
+  // K (activations, out of range, zeros), and is never consumed. The loop is
+  // unrolled by two so the current and next weight registers swap roles
+  // without copies.
+  auto step = [&](int kt, const uint16_t* cur, uint16_t* nxt, u32x4_t (&clo)[4], u32x4_t (&chi)[4],
+                  u32x4_t (&plo)[4], u32x4_t (&phi)[4]) {
+    const int kn = min(kt + 1, kt1 - 1);
+    load_x(kt + 1);
+    load_w_half(kn, 0, plo);
+    if (active) mma_half(cur, 0, clo);
+    load_w_half(kn, 1, phi);
+    if (active) mma_half(cur, 1, chi);
+    store_x(nxt);
     __syncthreads();
-    if (more) {
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        wlo[j] = nlo[j];
-        whi[j] = nhi[j];
-      }
-    }
+  };
+  load_x(kt0);
+  load_w_half(kt0, 0, wlo);
+  load_w_half(kt0, 1, whi);
+  store_x(lds0);
+  __syncthreads();
+  for (int kt = kt0; kt < kt1; kt += 2) {
+    step(kt, lds0, lds1, wlo, whi, nlo, nhi);
+    if (kt + 1 >= kt1) break;
+    step(kt + 1, lds1, lds0, nlo, nhi, wlo, whi);
   }
 
   if (!active) return;
@@ -314,6 +308,15 @@ __global__ void k_splitk_reduce(GemmArgs a) {
 
 size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k, 64) * 2; }
 
+static int gemm_variant() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = std::getenv("SIDP_GEMM_VARIANT");
+    v = e ? std::atoi(e) : 0;
+  }
+  return v;
+}
+
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int NG = round_up(n_cols_packed, 64) / 64;
   const int tiles = (NG + kWaves - 1) / kWaves;
@@ -369,20 +372,11 @@ static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
   return hipGetLastError();
 }
 
-static int gemm_variant() {
-  static int v = -1;
-  if (v < 0) {
-    const char* e = std::getenv("SIDP_GEMM_VARIANT");
-    v = e ? std::atoi(e) : 0;
-  }
-  return v;
-}
-
 template <int EPI, bool P>
 static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 32) return launch_mf<1, 1, EPI, P>(a, s);
   if (a.M <= 64) return launch_mf<2, 1, EPI, P>(a, s);
-  if (a.M <= 128 || gemm_variant() == 0) return launch_mf<4, 1, EPI, P>(a, s);
+  if (a.M <= 128 || gemm_variant() != 1) return launch_mf<4, 1, EPI, P>(a, s);
   return launch_mf<4, 2, EPI, P>(a, s);
 }
 
