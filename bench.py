@@ -55,7 +55,8 @@ def algorithmic_work(cfg, B, seq_total, layer_bytes):
         "qkv": (NQKV * H * 2 + B * H * 2 + B * NQKV * 2, 2 * B * NQKV * H),
         "rope_append": (B * NQKV * 2 + B * QD * 2 + B * kv_tok, 0),
         "attention": (seq_total * kv_tok + 2 * B * QD * 2, 4 * Hq * D * seq_total),
-        "o_proj": (H * QD * 2 + B * QD * 2 + 2 * B * H * 4, 2 * B * H * QD),
+        # the O projection's reduction also writes the FFN norm's bf16 output
+        "o_proj": (H * QD * 2 + B * QD * 2 + 2 * B * H * 4 + H * 2 + B * H * 2, 2 * B * H * QD),
         "norm_mlp": (B * H * 4 + H * 2 + B * H * 2, 0),
         "gate_up": (2 * F * H * 2 + B * H * 2 + B * F * 2, 2 * B * 2 * F * H),
         "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4, 2 * B * H * F),

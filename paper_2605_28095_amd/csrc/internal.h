@@ -20,6 +20,13 @@ struct LinearCall {
   float* ws;
   size_t ws_bytes;
   int num_cus;
+  // optional RMSNorm of the result (EPI_RESID in place only): norm_out = bf16(rmsnorm(out) * norm_gain)
+  const void* norm_gain = nullptr;
+  float norm_eps = 0.f;
+  void* norm_out = nullptr;
+  // leave split-K partials in ws for the consumer to reduce (it must sum them
+  // in split order and apply the epilogue); ignored when there is one split
+  bool defer_reduce = false;
 };
 
 size_t packed_bytes(int n, int k);
@@ -30,6 +37,9 @@ hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, voi
 hipError_t launch_linear(const LinearCall& c, hipStream_t s);
 
 hipError_t launch_rmsnorm(const float* x, const void* gain, float eps, void* out, int rows, int n, hipStream_t s);
+bool reduce_resid_norm_fits(int n);
+hipError_t launch_reduce_resid_norm(const float* ws, int splits, int M, int NP, int n, float* x, const void* gain,
+                                    float eps, void* h, hipStream_t s);
 
 struct KvView {
   uint16_t* k;            // [regions][nblk][Hkv][bs][D]
@@ -39,7 +49,10 @@ struct KvView {
 };
 
 struct RopeCall {
-  const uint16_t* qkv;
+  const uint16_t* qkv;    // bf16 projection output [B][heads * D], or
+  const float* ws;        // its split-K partials [splits][B][ws_np] (reduced here, in split order, + bias)
+  int splits, ws_np;
+  const uint16_t* bias;   // with ws only
   const int32_t* positions;
   const int32_t* block_tables;
   int max_blocks, batch;
@@ -68,13 +81,19 @@ struct AttnCall {
   KvView kv;
   int region;
   uint16_t* out;      // [B][Hq][D]
-  float* part;        // partials [B][Hq][max_parts][D + 2]
+  float* part;        // partials [B][Hq][max_parts][D + 4]: o[D], m, l, 2 pad
   int max_parts;
   uint32_t* err;
   int num_cus;
+  int32_t* plan;      // work list written by launch_attn_plan: [0] count, [1 + i] b | part << 16
 };
 int attn_part_tokens();
 size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq);
+size_t attn_plan_bytes(int max_batch, int max_parts);
+// Builds the work list from positions; needed once per set of positions (a
+// decode step shares it across its layers). Reads positions, batch,
+// max_blocks, kv.bs, plan, err.
+hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s);
 hipError_t launch_attention(const AttnCall& c, hipStream_t s);
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);

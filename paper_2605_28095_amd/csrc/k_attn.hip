@@ -1,8 +1,12 @@
 // Paged grouped-query decode attention on gfx950 (K4).
 //
-// Work is a flat list of items (sequence b, partition p, KV head g), a
-// partition being 1024 tokens; a persistent grid of 4-wave workgroups walks
-// the list. Within an item each wave owns 256 tokens, processed in chunks of
+// Work is a list of items (sequence b, partition p, KV head g), a partition
+// being 1024 tokens. A planning kernel, run once per set of positions, lists
+// the full partitions first and then each sequence's shorter last partition
+// by decreasing length; a persistent grid of 4-wave workgroups walks that
+// list in snake order (workgroup w takes items w, 2G - 1 - w, 2G + w, ...),
+// which keeps the workgroups' totals within about one short item of each
+// other. Within an item each wave owns 256 tokens, processed in chunks of
 // 32 tokens = two 16-token KV blocks, with the next chunk's K/V loads in
 // flight while the current one computes. The query heads of a KV group (up to
 // 16) ride in the MFMA's 16 columns, so every KV byte is read once for all of
@@ -29,7 +33,95 @@ int attn_part_tokens() { return kPartTokens; }
 
 size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq) {
   const int parts = (max_seq + kPartTokens - 1) / kPartTokens;
-  return (size_t)max_batch * hq * parts * (d + 2) * sizeof(float);
+  return (size_t)max_batch * hq * parts * (d + 4) * sizeof(float);
+}
+
+size_t attn_plan_bytes(int max_batch, int max_parts) { return (1 + (size_t)max_batch * max_parts) * sizeof(int32_t); }
+
+// The work list. plan[0] = number of (sequence, partition) entries; entry i is
+// plan[1 + i] = b | part << 16. Full 1024-token partitions come first, in
+// (b, part) order; then the last, shorter partition of every sequence that
+// has one, by decreasing length and then increasing b (a bitonic sort in
+// LDS). Positions outside a sequence's block table give no entries and set
+// the position error bit.
+__global__ void __launch_bounds__(256) k_attn_plan(const int32_t* __restrict__ positions, int batch, int np2,
+                                                   int max_tokens, int32_t* __restrict__ plan,
+                                                   uint32_t* __restrict__ err) {
+  extern __shared__ int lds_plan[];
+  int* s_key = lds_plan;     // [np2] tokens in the last partition (0: none)
+  int* s_b = s_key + np2;    // [np2] its sequence
+  int* s_full = s_b + np2;   // [batch] full partitions of each sequence
+  __shared__ int s_scan[256];
+  __shared__ int s_npart;
+  const int t = threadIdx.x;
+  if (t == 0) s_npart = 0;
+  __syncthreads();
+  for (int b = t; b < np2; b += 256) {
+    int full = 0, rem = 0;
+    if (b < batch) {
+      const int seq = positions[b] + 1;
+      if (seq >= 1 && seq <= max_tokens) {
+        full = seq / kPartTokens;
+        rem = seq % kPartTokens;
+      } else {
+        atomicOr(err, SIDP_DEVERR_POSITION);
+      }
+      s_full[b] = full;
+      if (rem > 0) atomicAdd(&s_npart, 1);
+    }
+    s_key[b] = rem;
+    s_b[b] = b;
+  }
+  __syncthreads();
+  // exclusive prefix of the full counts; thread t owns sequences [t * per, t * per + per)
+  const int per = (batch + 255) / 256;
+  int local = 0;
+  for (int i = 0; i < per; i++) {
+    const int b = t * per + i;
+    if (b < batch) local += s_full[b];
+  }
+  s_scan[t] = local;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int v = t >= off ? s_scan[t - off] : 0;
+    __syncthreads();
+    s_scan[t] += v;
+    __syncthreads();
+  }
+  int run = s_scan[t] - local;
+  for (int i = 0; i < per; i++) {
+    const int b = t * per + i;
+    if (b < batch) {
+      for (int p = 0; p < s_full[b]; p++) plan[1 + run + p] = b | (p << 16);
+      run += s_full[b];
+    }
+  }
+  const int nfull = s_scan[255];
+  // bitonic sort of (length descending, b ascending)
+  for (int k = 2; k <= np2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      __syncthreads();
+      for (int i = t; i < np2; i += 256) {
+        const int l = i ^ j;
+        if (l > i) {
+          const int ki = s_key[i], kl = s_key[l], bi = s_b[i], bl = s_b[l];
+          const bool i_first = ki > kl || (ki == kl && bi < bl);
+          if (((i & k) == 0) != i_first) {
+            s_key[i] = kl;
+            s_key[l] = ki;
+            s_b[i] = bl;
+            s_b[l] = bi;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = t; i < s_npart; i += 256) {
+    const int b = s_b[i];
+    plan[1 + nfull + i] = b | (s_full[b] << 16);
+  }
+  if (t == 0) plan[0] = nfull + s_npart;
 }
 
 template <int D>
@@ -169,46 +261,13 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
   float* s_m = smem_f;                             // [4][16]
   float* s_l = s_m + 64;                           // [4][16]
   float* s_o = s_l + 64;                           // [4][16][D + 1]
-  int* s_prefix = (int*)(s_o + 4 * 16 * (D + 1));  // [batch + 1]
-  __shared__ int s_scan[256];
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int head = lane & 15, lg = lane >> 4;
   const int group = a.hq / a.hkv;
-  const int B = a.batch;
 
-  // Exclusive prefix over sequences of their partition counts. Thread t owns
-  // sequences [t*per, t*per + per).
-  const int per = (B + 255) / 256;
-  int local = 0;
-  for (int i = 0; i < per; i++) {
-    const int b = threadIdx.x * per + i;
-    if (b < B) {
-      const int n = seq_parts(a, b);
-      if (n == 0 && blockIdx.x == 0) atomicOr(a.err, SIDP_DEVERR_POSITION);
-      local += n;
-    }
-  }
-  s_scan[threadIdx.x] = local;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {  // inclusive scan
-    const int v = threadIdx.x >= off ? s_scan[threadIdx.x - off] : 0;
-    __syncthreads();
-    s_scan[threadIdx.x] += v;
-    __syncthreads();
-  }
-  int run = s_scan[threadIdx.x] - local;
-  for (int i = 0; i < per; i++) {
-    const int b = threadIdx.x * per + i;
-    if (b < B) {
-      s_prefix[b] = run;
-      run += seq_parts(a, b);
-    }
-  }
-  if (threadIdx.x == 0) s_prefix[B] = s_scan[255];
-  __syncthreads();
-
-  const int total_items = s_prefix[B] * a.hkv;
+  cint32_t* plan = (cint32_t*)a.plan;
+  const int total_items = plan[0] * a.hkv;
   const float scale = kLog2e / sqrtf((float)D);
   const int64_t region_blk = (int64_t)a.region * a.kv.nblk;
   cint32_t* positions = (cint32_t*)a.positions;
@@ -219,21 +278,20 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     cint32_t* bt;
   };
   auto get_item = [&](int item, Item& it) {
-    const int pg = item / a.hkv;
+    const int e = plan[1 + item / a.hkv];
     it.g = item % a.hkv;
-    int lo_b = 0, hi_b = B - 1;  // last b with prefix[b] <= pg
-    while (lo_b < hi_b) {
-      const int mid = (lo_b + hi_b + 1) >> 1;
-      if (s_prefix[mid] <= pg) lo_b = mid;
-      else hi_b = mid - 1;
-    }
-    it.b = __builtin_amdgcn_readfirstlane(lo_b);
-    it.part = pg - s_prefix[it.b];
-    it.nparts = s_prefix[it.b + 1] - s_prefix[it.b];
+    it.b = e & 0xffff;
+    it.part = e >> 16;
     it.seq = positions[it.b] + 1;
+    it.nparts = (it.seq + kPartTokens - 1) / kPartTokens;
     it.bt = (cint32_t*)(a.block_tables + (int64_t)it.b * a.max_blocks);
     it.tb = it.part * kPartTokens + wave * kWaveTokens;
     it.te = min(it.tb + kWaveTokens, it.seq);
+  };
+  // the r-th item of this workgroup in snake order over the sorted list
+  auto item_of = [&](int r) {
+    const int G = gridDim.x;
+    return (r & 1) ? (r + 1) * G - 1 - (int)blockIdx.x : r * G + (int)blockIdx.x;
   };
   // Query heads ride in the 16 MFMA columns; lanes past the group load a
   // duplicate of the group's first head (finite values whose columns are never
@@ -251,7 +309,8 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
   const uint32_t k_lane = (uint32_t)(head * D + lg * 8) * 2u;
   const uint32_t v_lane = (uint32_t)(head * 16 + lg * 4) * 2u;
   bool bad = false;
-  int item = blockIdx.x;
+  int round = 0;
+  int item = item_of(0);
   if (item < total_items) {
     // The chunk stream of a wave runs across its items: the load slot after an
     // item's last chunk fetches the first chunk of the wave's part of the next
@@ -265,7 +324,7 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     Chunk<D> ca, cb;
     if (cur.tb < cur.te) load_chunk<D>(a, ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb}, region_blk, k_lane, v_lane, bad, ca);
     for (;;) {
-      const int nitem = item + gridDim.x;
+      const int nitem = item_of(round + 1);
       const bool has_next = nitem < total_items;
       Item nx = cur;
       if (has_next) get_item(nitem, nx);
@@ -322,7 +381,7 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
         if (cur.nparts == 1) {
           a.out[((int64_t)cur.b * a.hq + qh) * D + d] = f2bf(O / L);
         } else {
-          float* pp = a.part + (((int64_t)cur.b * a.hq + qh) * a.max_parts + cur.part) * (D + 2);
+          float* pp = a.part + (((int64_t)cur.b * a.hq + qh) * a.max_parts + cur.part) * (D + 4);
           pp[d] = O;
           if (d == 0) {
             pp[D] = M;
@@ -335,39 +394,61 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
       if ((n & 1) && pf) ca = cb;
       cur = nx;
       item = nitem;
+      round++;
     }
   }
   if (bad && lane == 0) atomicOr(a.err, SIDP_DEVERR_BLOCK);
 }
 
-// Log-sum-exp merge of a sequence's partitions: one workgroup per (head, b).
+// Log-sum-exp merge of a sequence's partitions: one workgroup per (KV head,
+// sequence) covering the group's query heads, four dims per thread (the
+// partial rows are padded to D + 4 floats so those loads are 16-byte
+// aligned). Partitions are summed in index order.
 template <int D>
-__global__ void __launch_bounds__(D) k_attn_combine(AttnCall a) {
-  const int qh = blockIdx.x, b = blockIdx.y;
+__global__ void __launch_bounds__(256) k_attn_combine(AttnCall a) {
+  constexpr int RS = D + 4;
+  const int g = blockIdx.x, b = blockIdx.y;
+  const int group = a.hq / a.hkv;
   const int nparts = seq_parts(a, b);
   if (nparts <= 1) return;
-  const float* p = a.part + ((int64_t)b * a.hq + qh) * a.max_parts * (D + 2);
-  float M = -INFINITY;
-  for (int i = 0; i < nparts; i++) M = fmaxf(M, p[i * (D + 2) + D]);
-  float L = 0.f, O = 0.f;
-  const int d = threadIdx.x;
-  for (int i = 0; i < nparts; i++) {
-    const float f = exp2f(p[i * (D + 2) + D] - M);
-    L += p[i * (D + 2) + D + 1] * f;
-    O += p[i * (D + 2) + d] * f;
+  for (int i = threadIdx.x; i < group * (D / 4); i += 256) {
+    const int qh = g * group + i / (D / 4), d = (i % (D / 4)) * 4;
+    const float* p = a.part + ((int64_t)b * a.hq + qh) * a.max_parts * RS;
+    float M = -INFINITY;
+    for (int j = 0; j < nparts; j++) M = fmaxf(M, p[j * RS + D]);
+    float L = 0.f;
+    f32x4_t O = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < nparts; j++) {
+      const float f = exp2f(p[j * RS + D] - M);
+      L += p[j * RS + D + 1] * f;
+      const f32x4_t v = *(const f32x4_t*)(p + j * RS + d);
+      O += v * f;
+    }
+    uint16_t* o = a.out + ((int64_t)b * a.hq + qh) * D + d;
+    *(uint32_t*)o = pack_bf2(O[0] / L, O[1] / L);
+    *(uint32_t*)(o + 2) = pack_bf2(O[2] / L, O[3] / L);
   }
-  a.out[((int64_t)b * a.hq + qh) * D + d] = f2bf(O / L);
+}
+
+hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s) {
+  if (c.batch <= 0) return hipSuccess;
+  int np2 = 1;
+  while (np2 < c.batch) np2 <<= 1;
+  const size_t lds = (size_t)(2 * np2 + c.batch) * sizeof(int);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  k_attn_plan<<<1, 256, lds, s>>>(c.positions, c.batch, np2, c.max_blocks * c.kv.bs, c.plan, c.err);
+  return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(const AttnCall& c, int grid, int parts, hipStream_t s) {
-  const size_t lds = (size_t)(128 + 4 * 16 * (D + 1)) * 4 + (size_t)(c.batch + 1) * 4;
+  const size_t lds = (size_t)(128 + 4 * 16 * (D + 1)) * 4;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)k_attn<D>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
   k_attn<D><<<grid, 256, lds, s>>>(c);
-  if (parts > 1) k_attn_combine<D><<<dim3(c.hq, c.batch), D, 0, s>>>(c);
+  if (parts > 1) k_attn_combine<D><<<dim3(c.hkv, c.batch), 256, 0, s>>>(c);
   return hipGetLastError();
 }
 

@@ -397,20 +397,29 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   a.resid = c.residual;
   a.ws = c.ws;
   if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
+  const bool fuse_norm = c.norm_out && c.epilogue == SIDP_EPI_RESID && c.residual == c.out;
+  if (c.norm_out && !fuse_norm) return hipErrorInvalidValue;
   hipError_t e;
   if (a.splits == 1) {
-    if (c.epilogue == SIDP_EPI_BF16) return launch_epi<SIDP_EPI_BF16, false>(a, s);
-    if (c.epilogue == SIDP_EPI_RESID) return launch_epi<SIDP_EPI_RESID, false>(a, s);
-    return launch_epi<SIDP_EPI_SWIGLU, false>(a, s);
+    if (c.epilogue == SIDP_EPI_BF16) e = launch_epi<SIDP_EPI_BF16, false>(a, s);
+    else if (c.epilogue == SIDP_EPI_RESID) e = launch_epi<SIDP_EPI_RESID, false>(a, s);
+    else e = launch_epi<SIDP_EPI_SWIGLU, false>(a, s);
+    if (e != hipSuccess || !fuse_norm) return e;
+    return launch_rmsnorm((const float*)c.out, c.norm_gain, c.norm_eps, c.norm_out, a.M, a.N, s);
   }
   e = launch_epi<SIDP_EPI_BF16, true>(a, s);  // partials only; epilogue in the reduction
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || c.defer_reduce) return e;
+  if (fuse_norm && reduce_resid_norm_fits(a.N))
+    return launch_reduce_resid_norm(a.ws, a.splits, a.M, a.NG * 64, a.N, (float*)c.out, c.norm_gain, c.norm_eps,
+                                    c.norm_out, s);
   const int64_t outs = (int64_t)a.M * a.N;
   const unsigned blocks = (unsigned)((outs + 255) / 256);
   if (c.epilogue == SIDP_EPI_BF16) k_splitk_reduce<SIDP_EPI_BF16><<<blocks, 256, 0, s>>>(a);
   else if (c.epilogue == SIDP_EPI_RESID) k_splitk_reduce<SIDP_EPI_RESID><<<blocks, 256, 0, s>>>(a);
   else k_splitk_reduce<SIDP_EPI_SWIGLU><<<blocks, 256, 0, s>>>(a);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !fuse_norm) return e;
+  return launch_rmsnorm((const float*)c.out, c.norm_gain, c.norm_eps, c.norm_out, a.M, a.N, s);
 }
 
 }  // namespace sidp

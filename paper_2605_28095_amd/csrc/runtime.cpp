@@ -137,6 +137,7 @@ struct sidp_handle {
   size_t ws_bytes = 0;
   float* attn_part = nullptr;
   int attn_max_parts = 0;
+  int32_t* attn_plan = nullptr;  // attention work list, rebuilt once per decode step
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
@@ -190,7 +191,7 @@ size_t sidp_layer_bytes(const sidp_config* cfg) {
 }
 
 static void free_device(sidp_handle* h) {
-  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->rope_cos, h->rope_sin, h->err};
+  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->rope_cos, h->rope_sin, h->err};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; i++) {
@@ -249,6 +250,7 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
       {(void**)&h->act, B * (size_t)c.ffn_dim * 2},
       {(void**)&h->ws, std::max<size_t>(ws, 256)},
       {(void**)&h->attn_part, std::max<size_t>(part_bytes, 256)},
+      {(void**)&h->attn_plan, attn_plan_bytes(c.max_batch, h->attn_max_parts)},
       {(void**)&h->rope_cos, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->rope_sin, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->err, 256},
@@ -461,13 +463,20 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   const int H = c.hidden, D = c.head_dim;
   // a2: RMSNorm before attention
   TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
-  // a3: QKV projection (+ bias)
-  TIMED(h, SIDP_K_QKV, s,
-        launch_linear(linear_call(h, h->h, B, H, wb + L.w_qkv, qkv_rows(c), SIDP_EPI_BF16,
-                                  c.qkv_bias ? wb + L.bias : nullptr, nullptr, h->qkv), s));
+  // a3: QKV projection (+ bias). With split-K its partials are reduced by the
+  // RoPE kernel below, which rounds to bf16 exactly where the projection would.
+  const uint16_t* qkv_bias = c.qkv_bias ? (const uint16_t*)(wb + L.bias) : nullptr;
+  LinearCall qc = linear_call(h, h->h, B, H, wb + L.w_qkv, qkv_rows(c), SIDP_EPI_BF16, qkv_bias, nullptr, h->qkv);
+  qc.defer_reduce = true;
+  const int qkv_splits = gemm_splits(B, qkv_rows(c), H, h->num_cus);
+  TIMED(h, SIDP_K_QKV, s, launch_linear(qc, s));
   // a4/a5: QK-norm, RoPE, KV append at the slot of each sequence's position
   RopeCall r;
   r.qkv = h->qkv;
+  r.ws = qkv_splits > 1 ? h->ws : nullptr;
+  r.splits = qkv_splits;
+  r.ws_np = round_up_i(qkv_rows(c), 64);
+  r.bias = qkv_bias;
   r.positions = positions;
   r.block_tables = bt;
   r.max_blocks = max_blocks;
@@ -503,6 +512,7 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   a.max_parts = h->attn_max_parts;
   a.err = h->err;
   a.num_cus = h->num_cus;
+  a.plan = h->attn_plan;
   TIMED(h, SIDP_K_ATTN, s, launch_attention(a, s));
   return hipSuccess;
 }
@@ -513,11 +523,13 @@ static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, float* hidden
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, QD = c.num_q_heads * c.head_dim;
-  // a7: O projection + residual (in place on the fp32 residual stream)
-  TIMED(h, SIDP_K_O, s,
-        launch_linear(linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden), s));
-  // a8: RMSNorm before the FFN
-  TIMED(h, SIDP_K_NORM_MLP, s, launch_rmsnorm(hidden, wb + L.g_mlp, c.rms_eps, h->h, B, H, s));
+  // a7 + a8: O projection + residual (in place on the fp32 residual stream),
+  // then the RMSNorm before the FFN, fused into the split-K reduction
+  LinearCall oc = linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
+  oc.norm_gain = wb + L.g_mlp;
+  oc.norm_eps = c.rms_eps;
+  oc.norm_out = h->h;
+  TIMED(h, SIDP_K_O, s, launch_linear(oc, s));
   // a9: gate/up projection + SwiGLU
   TIMED(h, SIDP_K_GATE_UP, s,
         launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
@@ -573,6 +585,17 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   hipStream_t cs = (hipStream_t)compute, cp = (hipStream_t)copy;
   if (streamed && (!h->slots || cp == cs)) return SIDP_EINVAL;
   h->last_compute = cs;
+  {
+    // the attention work list depends on the positions only: one per step
+    AttnCall a{};
+    a.positions = positions;
+    a.batch = batch;
+    a.max_blocks = max_blocks_per_seq;
+    a.kv = kv_view(h);
+    a.plan = h->attn_plan;
+    a.err = h->err;
+    HIPCHK(h, launch_attn_plan(a, cs));
+  }
 
   if (!streamed) {
     for (int l = 0; l < c.num_layers; l++)
@@ -742,6 +765,10 @@ int sidp_rope_append(sidp_handle* h, const void* qkv, const int32_t* positions, 
   if (h->cfg.qk_norm && (!g_q || !g_k)) return SIDP_EINVAL;
   RopeCall r;
   r.qkv = (const uint16_t*)qkv;
+  r.ws = nullptr;
+  r.splits = 1;
+  r.ws_np = 0;
+  r.bias = nullptr;
   r.positions = positions;
   r.block_tables = block_tables;
   r.max_blocks = max_blocks_per_seq;
@@ -787,6 +814,8 @@ int sidp_attention(sidp_handle* h, const void* q, int32_t region, const int32_t*
   a.max_parts = h->attn_max_parts;
   a.err = h->err;
   a.num_cus = h->num_cus;
+  a.plan = h->attn_plan;
+  HIPCHK(h, launch_attn_plan(a, (hipStream_t)stream));
   HIPCHK(h, launch_attention(a, (hipStream_t)stream));
   h->last_compute = (hipStream_t)stream;
   return SIDP_OK;
