@@ -59,7 +59,8 @@ def algorithmic_work(cfg, B, seq_total, layer_bytes):
         "o_proj": (H * QD * 2 + B * QD * 2 + 2 * B * H * 4 + H * 2 + B * H * 2, 2 * B * H * QD),
         "norm_mlp": (B * H * 4 + H * 2 + B * H * 2, 0),
         "gate_up": (2 * F * H * 2 + B * H * 2 + B * F * 2, 2 * B * 2 * F * H),
-        "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4, 2 * B * H * F),
+        # and the down projection's reduction writes the next layer's attention-norm output
+        "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4 + H * 2 + B * H * 2, 2 * B * H * F),
         "fill": (2 * layer_bytes, 0),
         "wait_fill": (0, 0),
     }

@@ -30,7 +30,7 @@ namespace {
 constexpr int kSlots = 2;
 constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
-constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
+constexpr int kFillPartAPercent = 35;  // share of a layer's fill issued before its predecessor's attention
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
@@ -138,6 +138,10 @@ struct sidp_handle {
   float* attn_part = nullptr;
   int attn_max_parts = 0;
   int32_t* attn_plan = nullptr;  // attention work list, rebuilt once per decode step
+  // The attention-norm gains of every layer ([L][H] bf16, 16 KB per layer at
+  // H = 8192), kept resident beside the pool so that layer l's down-projection
+  // reduction can apply layer l + 1's norm before layer l + 1's slot is read.
+  uint16_t* g_attn_all = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
@@ -191,7 +195,7 @@ size_t sidp_layer_bytes(const sidp_config* cfg) {
 }
 
 static void free_device(sidp_handle* h) {
-  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->rope_cos, h->rope_sin, h->err};
+  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->g_attn_all, h->rope_cos, h->rope_sin, h->err};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; i++) {
@@ -251,6 +255,7 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
       {(void**)&h->ws, std::max<size_t>(ws, 256)},
       {(void**)&h->attn_part, std::max<size_t>(part_bytes, 256)},
       {(void**)&h->attn_plan, attn_plan_bytes(c.max_batch, h->attn_max_parts)},
+      {(void**)&h->g_attn_all, (size_t)c.num_layers * H * 2},
       {(void**)&h->rope_cos, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->rope_sin, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->err, 256},
@@ -321,6 +326,7 @@ int sidp_pool_load_layer(sidp_handle* h, int32_t layer, const sidp_layer_weights
   uint8_t* base = h->pool + (size_t)layer * h->blob.total;
   const size_t H = c.hidden, D = c.head_dim, QD = (size_t)c.num_q_heads * D, KD = (size_t)c.num_kv_heads * D;
   HIPCHK(h, hipMemcpyAsync(base + h->blob.g_attn, w->g_attn, H * 2, hipMemcpyDeviceToDevice, s));
+  HIPCHK(h, hipMemcpyAsync(h->g_attn_all + (size_t)layer * H, w->g_attn, H * 2, hipMemcpyDeviceToDevice, s));
   HIPCHK(h, hipMemcpyAsync(base + h->blob.g_mlp, w->g_mlp, H * 2, hipMemcpyDeviceToDevice, s));
   if (c.qk_norm) {
     HIPCHK(h, hipMemcpyAsync(base + h->blob.g_q, w->g_q, D * 2, hipMemcpyDeviceToDevice, s));
@@ -461,8 +467,9 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, D = c.head_dim;
-  // a2: RMSNorm before attention
-  TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
+  // a2: RMSNorm before attention; for layers after the first of a step the
+  // previous layer's down-projection reduction has already written it
+  if (layer == 0) TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
   // a3: QKV projection (+ bias). With split-K its partials are reduced by the
   // RoPE kernel below, which rounds to bf16 exactly where the projection would.
   const uint16_t* qkv_bias = c.qkv_bias ? (const uint16_t*)(wb + L.bias) : nullptr;
@@ -519,7 +526,7 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
 
 // The projection half of a layer (O + residual, norm, gate/up + SwiGLU,
 // down + residual).
-static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, float* hidden, int B, hipStream_t s) {
+static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, int B, hipStream_t s) {
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, QD = c.num_q_heads * c.head_dim;
@@ -534,10 +541,15 @@ static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, float* hidden
   TIMED(h, SIDP_K_GATE_UP, s,
         launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
                       s));
-  // a10: down projection + residual
-  TIMED(h, SIDP_K_DOWN, s,
-        launch_linear(linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden),
-                      s));
+  // a10: down projection + residual, fused with the next layer's attention
+  // norm (a2 of layer + 1) when there is a next layer in this step
+  LinearCall dc = linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
+  if (layer + 1 < c.num_layers) {
+    dc.norm_gain = h->g_attn_all + (size_t)(layer + 1) * H;
+    dc.norm_eps = c.rms_eps;
+    dc.norm_out = h->h;
+  }
+  TIMED(h, SIDP_K_DOWN, s, launch_linear(dc, s));
   return hipSuccess;
 }
 
@@ -545,7 +557,7 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
                             const int32_t* bt, int max_blocks, int B, hipStream_t s) {
   hipError_t e = run_attn_half(h, wb, layer, hidden, positions, bt, max_blocks, B, s);
   if (e != hipSuccess) return e;
-  return run_proj_half(h, wb, hidden, B, s);
+  return run_proj_half(h, wb, layer, hidden, B, s);
 }
 
 // Part of one slot fill on the copy stream: bytes [lo, hi) of layer (g mod L)
@@ -642,7 +654,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         HIPCHK(h, hipEventRecord(h->mid[op.slot], cs));
         break;
       case OP_PROJ:
-        HIPCHK(h, run_proj_half(h, slot, hidden, batch, cs));
+        HIPCHK(h, run_proj_half(h, slot, (int)(op.g % c.num_layers), hidden, batch, cs));
         break;
       case OP_DONE:
         HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
