@@ -42,9 +42,20 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_work(cfg, B, seq_total, layer_bytes):
-    """Bytes and flops each kernel class must move / perform for one layer at
-    batch B (seq_total = sum over sequences of attended tokens)."""
+def staged_bytes(cfg, layer_bytes, pooling):
+    """Bytes of a layer blob a slot fill copies: the whole blob, or its FFN part
+    (FFN norm gain, packed gate/up and down projections, 256-byte aligned)."""
+    if pooling == "layer":
+        return layer_bytes
+    H, F = cfg["hidden"], cfg["ffn_dim"]
+    r = lambda a, b: -(-a // b) * b  # noqa: E731
+    return r(H * 2, 256) + r(r(2 * r(F, 32), 64) * r(H, 64) * 2, 256) + r(r(H, 64) * r(F, 64) * 2, 256)
+
+
+def algorithmic_work(cfg, B, seq_total, fill_bytes):
+    """Bytes and flops each kernel class must move / perform for one launch at
+    batch B (seq_total = sum over sequences of attended tokens); a layer's fill
+    is two launches that together read and write fill_bytes."""
     H, D, F = cfg["hidden"], cfg["head_dim"], cfg["ffn_dim"]
     Hq, Hkv = cfg["num_q_heads"], cfg["num_kv_heads"]
     QD, KD = Hq * D, Hkv * D
@@ -61,7 +72,7 @@ def algorithmic_work(cfg, B, seq_total, layer_bytes):
         "gate_up": (2 * F * H * 2 + B * H * 2 + B * F * 2, 2 * B * 2 * F * H),
         # and the down projection's reduction writes the next layer's attention-norm output
         "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4 + H * 2 + B * H * 2, 2 * B * H * F),
-        "fill": (2 * layer_bytes, 0),
+        "fill": (fill_bytes, 0),  # per launch: 2 x fill_bytes over the layer's two tiles
         "wait_fill": (0, 0),
     }
     return w
@@ -126,6 +137,10 @@ def main():
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--mode", choices=["streamed", "resident"], default="streamed")
     ap.add_argument("--copy", choices=["background", "burst", "memcpy"], default="background")
+    ap.add_argument("--pooling", choices=["layer", "ffn"], default="layer",
+                    help="stage whole layers, or only their FFN part (attention weights read in place)")
+    ap.add_argument("--ranks", type=int, default=0, help="pooling ranks d: layers l with l %% d == rank are owned")
+    ap.add_argument("--rank", type=int, default=0)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -216,6 +231,7 @@ def main():
     elif args.copy == "burst":
         flags |= sidp.SIDP_COPY_BURST
 
+    dec.set_pooling(sidp.SIDP_POOL_FFN if args.pooling == "ffn" else sidp.SIDP_POOL_LAYER, args.ranks, args.rank)
     for i in range(args.warmup):
         dec.step(hidden, pos, bt, flags, compute=compute, copy=copy_stream)
     dec.sync()
@@ -240,7 +256,8 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step, {value:.1f} tok/s (wall {wall:.2f}s)")
 
     seq_total = int(ctx.sum()) + B
-    work = algorithmic_work(cfg, B, seq_total, layer_bytes)
+    fill_bytes = staged_bytes(cfg, layer_bytes, args.pooling)
+    work = algorithmic_work(cfg, B, seq_total, fill_bytes)
     kernels = {}
     for name, (ms, n) in timing.items():
         if n == 0:
@@ -300,7 +317,8 @@ def main():
             "workload": f"{args.workload}: {DESCR.get(args.workload, args.workload)}",
             "global_batch": B, "layers": L, "seq_len": f"ctx U[{cfg['ctx_lo']},{cfg['ctx_hi']}], mean {ctx.mean():.0f}",
             "parallelism": "single GPU", "mode": args.mode, "copy": args.copy, "kv_regions": R,
-            "layer_bytes": layer_bytes,
+            "layer_bytes": layer_bytes, "pooling": args.pooling, "staged_bytes": fill_bytes,
+            "owned_layers": sum(1 for l in range(L) if args.ranks > 0 and l % args.ranks == args.rank),
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

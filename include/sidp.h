@@ -61,14 +61,14 @@ extern "C" {
 #define SIDP_TIMING        0x40 /* bracket each kernel class with HIP events (sidp_timing_collect) */
 
 /* ---- kernel classes timed under SIDP_TIMING ---- */
-#define SIDP_K_NORM_ATTN  0 /* RMSNorm before attention              */
-#define SIDP_K_QKV        1 /* QKV projection (+bias)                 */
-#define SIDP_K_ROPE       2 /* QK-norm + RoPE + KV append             */
-#define SIDP_K_ATTN       3 /* paged attention (+ partition combine)  */
-#define SIDP_K_O          4 /* O projection + residual                */
-#define SIDP_K_NORM_MLP   5 /* RMSNorm before the FFN                 */
-#define SIDP_K_GATE_UP    6 /* gate/up projection + SwiGLU            */
-#define SIDP_K_DOWN       7 /* down projection + residual             */
+#define SIDP_K_NORM_ATTN  0 /* RMSNorm before attention (first layer of a step) */
+#define SIDP_K_QKV        1 /* QKV projection (+bias), split-K partials       */
+#define SIDP_K_ROPE       2 /* QKV reduce + QK-norm + RoPE + KV append         */
+#define SIDP_K_ATTN       3 /* paged attention (+ partition combine)           */
+#define SIDP_K_O          4 /* O projection + residual + RMSNorm before the FFN */
+#define SIDP_K_NORM_MLP   5 /* RMSNorm before the FFN when not fused (unused)  */
+#define SIDP_K_GATE_UP    6 /* gate/up projection + SwiGLU                     */
+#define SIDP_K_DOWN       7 /* down projection + residual (+ next layer's attention RMSNorm) */
 #define SIDP_K_FILL       8 /* slot fill (copy stream)                */
 #define SIDP_K_WAIT_FILL  9 /* compute stream blocked on a slot fill  */
 #define SIDP_NUM_KCLASSES 10
@@ -200,22 +200,43 @@ int sidp_sync(sidp_handle *h);
  * brackets one layer's launches of that class on the stream they run on. */
 int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
 
+/* ---- pooling ----
+ * What the weight cache stages, and which layers this rank owns (§4.1: each
+ * rank keeps the FFN weights of the layers it owns in its pool and reads the
+ * others from their owners; attention weights stay with every replica).
+ *   mode  SIDP_POOL_LAYER: a streamed layer's whole blob is staged (default);
+ *         SIDP_POOL_FFN: only its FFN part (norm gain, gate/up, down) is
+ *         staged, its attention part is read from the pool in place.
+ *   ranks, rank: with ranks > 0, layer l with l % ranks == rank is owned and
+ *         computed straight from the pool in streamed steps (no slot, no
+ *         copy); ranks = 0 owns no layer (default). 0 <= rank < ranks.
+ * On one GPU the pool stands in for both this rank's pool and the owners' pools
+ * of the layers it streams. Restarts the slot ring; call it only when no step
+ * is in flight on the handle (after sidp_sync). SIDP_EINVAL on bad arguments. */
+#define SIDP_POOL_LAYER 0
+#define SIDP_POOL_FFN   1
+int sidp_set_pooling(sidp_handle *h, int32_t mode, int32_t ranks, int32_t rank);
+
 /* ---- the slot-ring plan (host only) ----
- * The order in which sidp_decode_step issues its ring operations on the two
- * streams, for `steps` streamed calls of num_layers layers with 2 slots. Layer
- * g (counted across calls) computes from slot g % 2 while layer g + 1 is
- * copied into the other slot as two tiles (§4.2 "tensor tiles", each with its
- * notification): tile A once layer g - 1 has released the slot, tile B once
- * layer g's attention half has been issued, so that it runs beside layer g's
- * projections. Each op is 3 int32 {kind, layer g, slot}; kinds:
+ * The order in which sidp_decode_step issues its operations on the two
+ * streams, for `steps` streamed calls of num_layers layers with 2 slots, on
+ * rank `rank` of `ranks` pooling ranks (ranks = 0: no owned layers; see
+ * sidp_set_pooling). Streamed layers are counted across calls by g (g-th
+ * non-owned layer instance): layer g computes from slot g % 2 while layer
+ * g + 1 is copied into the other slot as two tiles (§4.2 "tensor tiles", each
+ * with its notification): tile A once layer g - 1 has released the slot, tile
+ * B once layer g's attention half has been issued, so that it runs beside
+ * layer g's projections. Each op is 3 int32 {kind, g, slot}; kinds:
  *   0 copy tile A of layer g          1 copy tile B of layer g, then mark filled
  *   2 compute waits for the fill      3 attention half of layer g
  *   4 mark attention half issued      5 projection half of layer g
  *   6 mark slot released              7 copy stream waits for the release
- *   8 copy stream waits for the attention half.
+ *   8 copy stream waits for the attention half
+ *   9 an owned layer computed from the pool; g = call * num_layers + layer, slot -1.
  * ops (host, 3 * *n_ops int32) receives up to *n_ops ops; on return *n_ops is
- * the number written. SIDP_EINVAL if the capacity is too small. */
-int sidp_plan(int32_t num_layers, int32_t steps, int32_t *ops, int32_t *n_ops);
+ * the number written. SIDP_EINVAL if the capacity is too small or the
+ * arguments are bad. */
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, int32_t *ops, int32_t *n_ops);
 
 /* ---- single kernels, for parity checks and reuse ----
  * All enqueue on `stream` and return immediately. */

@@ -19,6 +19,14 @@ compute waits for tile B's notification. Before the first layer, layer 0 is
 read whole. The copy stream therefore always runs one layer ahead, also across
 the end of an iteration.
 
+Layers owned by this rank (§4.1: each rank keeps the FFN weights of the
+layers it owns, layer l being owned by rank l mod d when d ranks pool their
+weights) are computed straight from the local pool: no read, no slot. The
+ring above then runs over the layers this rank does not own, g counting only
+those (g = step * Ls + j for the j-th non-owned layer of a step, Ls of them
+per step), and an owned layer's compute sits between the ring operations of
+its neighbours in layer order.
+
 Operations, in host issue order, as (kind, g, slot):
   ("fill_a", g, s)     copy tile A of layer g mod L into slot s
   ("fill_b", g, s)     copy tile B, then notify "filled"
@@ -29,21 +37,39 @@ Operations, in host issue order, as (kind, g, slot):
   ("done", g, s)       compute notifies that slot s is free
   ("wait_done", g, s)  copy waits for layer g's "done"
   ("wait_mid", g, s)   copy waits for layer g's "mid"
+  ("local", n, -1)     compute of owned layer n (n = step * L + l), from the pool
 """
 
 
-def was_schedule(num_layers, steps):
+def owned(layer, ranks, rank):
+    """Whether this rank owns `layer` (ranks = 0: it owns none)."""
+    return ranks > 0 and layer % ranks == rank
+
+
+def was_schedule(num_layers, steps, ranks=0, rank=0):
     """Issue order of the ring operations for `steps` decode iterations of
-    `num_layers` layers."""
-    total = num_layers * steps
+    `num_layers` layers, on rank `rank` of `ranks` pooling ranks."""
+    streamed = [l for l in range(num_layers) if not owned(l, ranks, rank)]
+    total = len(streamed) * steps
     ops = []
-    if total == 0:
-        return ops
-    ops += [("fill_a", 0, 0), ("fill_b", 0, 0)]
-    for g in range(total):
-        s, n = g % 2, (g + 1) % 2
-        if g > 0:
-            ops.append(("wait_done", g - 1, n))
-        ops += [("fill_a", g + 1, n), ("wait_fill", g, s), ("attn", g, s), ("mid", g, s),
-                ("wait_mid", g, s), ("fill_b", g + 1, n), ("proj", g, s), ("done", g, s)]
+    if total > 0:
+        ops += [("fill_a", 0, 0), ("fill_b", 0, 0)]
+    g = 0
+    for step in range(steps):
+        for l in range(num_layers):
+            if owned(l, ranks, rank):
+                ops.append(("local", step * num_layers + l, -1))
+                continue
+            s, n = g % 2, (g + 1) % 2
+            if g > 0:
+                ops.append(("wait_done", g - 1, n))
+            ops += [("fill_a", g + 1, n), ("wait_fill", g, s), ("attn", g, s), ("mid", g, s),
+                    ("wait_mid", g, s), ("fill_b", g + 1, n), ("proj", g, s), ("done", g, s)]
+            g += 1
     return ops
+
+
+def streamed_layer(g, num_layers, ranks=0, rank=0):
+    """The layer (0 .. L-1) that ring instance g computes."""
+    streamed = [l for l in range(num_layers) if not owned(l, ranks, rank)]
+    return streamed[g % len(streamed)]

@@ -38,14 +38,17 @@ SIDP_EPI_RESID = 1
 SIDP_EPI_SWIGLU = 2
 
 PLAN_OPS = {0: "fill_a", 1: "fill_b", 2: "wait_fill", 3: "attn", 4: "mid", 5: "proj", 6: "done", 7: "wait_done",
-            8: "wait_mid"}
+            8: "wait_mid", 9: "local"}
+
+SIDP_POOL_LAYER = 0
+SIDP_POOL_FFN = 1
 
 EXPORTED = [
     "sidp_strerror", "sidp_last_hip_error", "sidp_create", "sidp_destroy", "sidp_layer_bytes",
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
-    "sidp_timing_collect",
+    "sidp_timing_collect", "sidp_set_pooling",
 ]
 
 
@@ -94,7 +97,8 @@ _sigs = {
     "sidp_kv_attach": (ctypes.c_int, [_P, _P, _P, _I, _I]),
     "sidp_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _I, _P, _P]),
     "sidp_sync": (ctypes.c_int, [_P]),
-    "sidp_plan": (ctypes.c_int, [_I, _I, _PI, _PI]),
+    "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
+    "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
     "sidp_rmsnorm": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I, _I, _P]),
     "sidp_packed_bytes": (_Z, [_I, _I]),
     "sidp_pack_linear": (ctypes.c_int, [_P, _I, _I, _P, _P]),
@@ -205,13 +209,17 @@ def sidp_sync(h):
     _check(_lib.sidp_sync(h), "sidp_sync")
 
 
-def sidp_plan(num_layers, steps):
-    """Ring operations in issue order, as (kind name, layer g, slot)."""
+def sidp_plan(num_layers, steps, ranks=0, rank=0):
+    """Ring operations in issue order, as (kind name, g, slot)."""
     cap = 9 * num_layers * steps + 2
     buf = (ctypes.c_int32 * (3 * cap))()
     n = ctypes.c_int32(cap)
-    _check(_lib.sidp_plan(num_layers, steps, buf, ctypes.byref(n)), "sidp_plan")
+    _check(_lib.sidp_plan(num_layers, steps, ranks, rank, buf, ctypes.byref(n)), "sidp_plan")
     return [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n.value)]
+
+
+def sidp_set_pooling(h, mode, ranks=0, rank=0):
+    _check(_lib.sidp_set_pooling(h, mode, ranks, rank), "sidp_set_pooling")
 
 
 def sidp_rmsnorm(x, gain, eps, out, rows, n, stream=None):

@@ -35,8 +35,11 @@ constexpr int kFillPartAPercent = 35;  // share of a layer's fill issued before 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
 
+// A layer's blob: the attention part (norm gain, QK-norm gains, QKV bias, QKV
+// and O projections), then the FFN part from `ffn_lo` on (FFN norm gain,
+// gate/up, down), so that FFN-only pooling stages one contiguous range.
 struct BlobLayout {
-  size_t g_attn, g_mlp, g_q, g_k, bias, w_qkv, w_o, w_gu, w_d, total;
+  size_t g_attn, g_q, g_k, bias, w_qkv, w_o, ffn_lo, g_mlp, w_gu, w_d, total;
 };
 
 int qkv_rows(const sidp_config& c) { return (c.num_q_heads + 2 * c.num_kv_heads) * c.head_dim; }
@@ -46,12 +49,13 @@ BlobLayout blob_layout(const sidp_config& c) {
   size_t o = 0;
   const size_t H = (size_t)c.hidden, D = (size_t)c.head_dim;
   b.g_attn = o; o = align_up(o + H * 2, kAlign);
-  b.g_mlp = o;  o = align_up(o + H * 2, kAlign);
   b.g_q = o;    o = align_up(o + (c.qk_norm ? D * 2 : 0), kAlign);
   b.g_k = o;    o = align_up(o + (c.qk_norm ? D * 2 : 0), kAlign);
   b.bias = o;   o = align_up(o + (c.qkv_bias ? (size_t)qkv_rows(c) * 2 : 0), kAlign);
   b.w_qkv = o;  o = align_up(o + packed_bytes(qkv_rows(c), c.hidden), kAlign);
   b.w_o = o;    o = align_up(o + packed_bytes(c.hidden, c.num_q_heads * c.head_dim), kAlign);
+  b.ffn_lo = o;
+  b.g_mlp = o;  o = align_up(o + H * 2, kAlign);
   b.w_gu = o;   o = align_up(o + packed_bytes(2 * round_up_i(c.ffn_dim, 32), c.hidden), kAlign);
   b.w_d = o;    o = align_up(o + packed_bytes(c.hidden, c.ffn_dim), kAlign);
   b.total = o;
@@ -88,6 +92,7 @@ enum {
   OP_DONE = 6,       // compute: mark the slot released
   OP_WAIT_DONE = 7,  // copy stream waits for layer g to release its slot
   OP_WAIT_MID = 8,   // copy stream waits for layer g's attention half
+  OP_LOCAL = 9,      // compute: a layer this rank owns, straight from the pool (g = step * L + layer)
 };
 struct RingOp {
   int kind;
@@ -111,6 +116,31 @@ void ring_layer(int64_t g, bool first, std::vector<RingOp>& ops) {
   ops.push_back({OP_FILL_B, g + 1, n});
   ops.push_back({OP_PROJ, g, s});
   ops.push_back({OP_DONE, g, s});
+}
+
+bool layer_owned(int l, int ranks, int rank) { return ranks > 0 && l % ranks == rank; }
+
+// The operations of one decode step over layers 0 .. L-1. Layers this rank
+// owns are computed from the pool (OP_LOCAL, g = step * L + l); the others go
+// through the ring, whose counter and started flag carry across steps.
+void build_step(int L, int ranks, int rank, int64_t step, int64_t* ring_g, bool* ring_started,
+                std::vector<RingOp>& ops) {
+  bool any_streamed = false;
+  for (int l = 0; l < L; l++) any_streamed |= !layer_owned(l, ranks, rank);
+  bool first = false;
+  if (any_streamed && !*ring_started) {
+    ring_prologue(*ring_g, ops);
+    *ring_started = true;
+    first = true;
+  }
+  for (int l = 0; l < L; l++) {
+    if (layer_owned(l, ranks, rank)) {
+      ops.push_back({OP_LOCAL, step * L + l, -1});
+      continue;
+    }
+    ring_layer((*ring_g)++, first, ops);
+    first = false;
+  }
 }
 
 }  // namespace
@@ -145,7 +175,11 @@ struct sidp_handle {
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
-  size_t fill_split = 0;  // bytes of a layer blob in fill part A
+  int fill_pct = 0;       // percent of the staged range in fill part A
+  // pooling: which part of a layer is staged, and which layers this rank owns
+  int pool_mode = SIDP_POOL_LAYER;
+  int ranks = 0, rank = 0;          // layer l is owned (never staged) when ranks > 0 and l % ranks == rank
+  std::vector<int> streamed_layers;  // the layers that are staged, in order
   bool events_ok = false;
   // ring state
   bool ring_started = false;
@@ -279,12 +313,9 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
     if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->mid[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
   }
-  {
-    int pct = kFillPartAPercent;
-    if (const char* e = std::getenv("SIDP_FILL_SPLIT")) pct = std::min(100, std::max(0, std::atoi(e)));
-    h->fill_split = align_up(h->blob.total * (size_t)pct / 100, kAlign);
-    if (h->fill_split > h->blob.total) h->fill_split = h->blob.total;
-  }
+  h->fill_pct = kFillPartAPercent;
+  if (const char* e = std::getenv("SIDP_FILL_SPLIT")) h->fill_pct = std::min(100, std::max(0, std::atoi(e)));
+  for (int l = 0; l < c.num_layers; l++) h->streamed_layers.push_back(l);
   *out = h;
   return SIDP_OK;
 }
@@ -526,24 +557,27 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
 
 // The projection half of a layer (O + residual, norm, gate/up + SwiGLU,
 // down + residual).
-static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wb, int layer, float* hidden, int B, hipStream_t s) {
+// `wa` holds the layer's attention part (W_o), `wf` its FFN part; both are
+// the same blob unless only the FFN part is staged.
+static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wa, const uint8_t* wf, int layer, float* hidden, int B,
+                                hipStream_t s) {
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, QD = c.num_q_heads * c.head_dim;
   // a7 + a8: O projection + residual (in place on the fp32 residual stream),
   // then the RMSNorm before the FFN, fused into the split-K reduction
-  LinearCall oc = linear_call(h, h->o, B, QD, wb + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
-  oc.norm_gain = wb + L.g_mlp;
+  LinearCall oc = linear_call(h, h->o, B, QD, wa + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
+  oc.norm_gain = wf + L.g_mlp;
   oc.norm_eps = c.rms_eps;
   oc.norm_out = h->h;
   TIMED(h, SIDP_K_O, s, launch_linear(oc, s));
   // a9: gate/up projection + SwiGLU
   TIMED(h, SIDP_K_GATE_UP, s,
-        launch_linear(linear_call(h, h->h, B, H, wb + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
+        launch_linear(linear_call(h, h->h, B, H, wf + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
                       s));
   // a10: down projection + residual, fused with the next layer's attention
   // norm (a2 of layer + 1) when there is a next layer in this step
-  LinearCall dc = linear_call(h, h->act, B, c.ffn_dim, wb + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
+  LinearCall dc = linear_call(h, h->act, B, c.ffn_dim, wf + L.w_d, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
   if (layer + 1 < c.num_layers) {
     dc.norm_gain = h->g_attn_all + (size_t)(layer + 1) * H;
     dc.norm_eps = c.rms_eps;
@@ -557,19 +591,32 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
                             const int32_t* bt, int max_blocks, int B, hipStream_t s) {
   hipError_t e = run_attn_half(h, wb, layer, hidden, positions, bt, max_blocks, B, s);
   if (e != hipSuccess) return e;
-  return run_proj_half(h, wb, layer, hidden, B, s);
+  return run_proj_half(h, wb, wb, layer, hidden, B, s);
 }
 
-// Part of one slot fill on the copy stream: bytes [lo, hi) of layer (g mod L)
-// from the pool into `slot`. The debug poison and delay precede the first part.
+// The staged byte range [lo, hi) of a layer blob and the end `mid` of fill part A.
+static void staged_range(const sidp_handle* h, size_t* lo, size_t* mid, size_t* hi) {
+  *lo = h->pool_mode == SIDP_POOL_FFN ? h->blob.ffn_lo : 0;
+  *hi = h->blob.total;
+  *mid = std::min(*hi, *lo + align_up((*hi - *lo) * (size_t)h->fill_pct / 100, kAlign));
+}
+
+// The layer that ring instance g computes.
+static int ring_layer_index(const sidp_handle* h, int64_t g) {
+  return h->streamed_layers[(size_t)(g % (int64_t)h->streamed_layers.size())];
+}
+
+// Part of one slot fill on the copy stream: bytes [lo, hi) of the blob of
+// ring instance g's layer, from the pool into slot `slot`.
 static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, size_t hi, int flags, hipStream_t cp) {
   const size_t lb = h->blob.total;
   uint8_t* dst = h->slots + (size_t)slot * lb;
-  const uint8_t* src = h->pool + (size_t)(g % h->cfg.num_layers) * lb;
+  const uint8_t* src = h->pool + (size_t)ring_layer_index(h, g) * lb;
+  const bool part_a = lo == (h->pool_mode == SIDP_POOL_FFN ? h->blob.ffn_lo : 0);
   hipError_t e;
-  if (lo == 0 && (flags & SIDP_DEBUG_POISON))
+  if (part_a && (flags & SIDP_DEBUG_POISON))  // the whole slot, unstaged parts included
     if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
-  if (lo == 0 && (flags & SIDP_DEBUG_DELAY))
+  if (part_a && (flags & SIDP_DEBUG_DELAY))
     if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
   if (hi <= lo) return hipSuccess;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
@@ -619,25 +666,21 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   h->last_copy = cp;
   h->any_copy = true;
   std::vector<RingOp> ops;
-  bool first = false;
-  if (!h->ring_started) {
-    ring_prologue(h->ring_g, ops);
-    h->ring_started = true;
-    first = true;
-  }
-  for (int l = 0; l < c.num_layers; l++) {
-    const int64_t g = h->ring_g++;
-    ring_layer(g, first && l == 0, ops);
-  }
+  build_step(c.num_layers, h->ranks, h->rank, 0, &h->ring_g, &h->ring_started, ops);
   const size_t lb = h->blob.total;
+  size_t st_lo, st_mid, st_hi;
+  staged_range(h, &st_lo, &st_mid, &st_hi);
+  const bool ffn_only = h->pool_mode == SIDP_POOL_FFN;
   for (const RingOp& op : ops) {
-    const uint8_t* slot = h->slots + (size_t)op.slot * lb;
+    const uint8_t* slot = op.slot >= 0 ? h->slots + (size_t)op.slot * lb : nullptr;
+    const int layer = op.kind == OP_LOCAL ? (int)(op.g % c.num_layers) : ring_layer_index(h, op.g);
+    const uint8_t* own = h->pool + (size_t)layer * lb;  // the layer's blob in the pool
     switch (op.kind) {
       case OP_FILL_A:
-        HIPCHK(h, issue_fill(h, op.g, op.slot, 0, h->fill_split, flags, cp));
+        HIPCHK(h, issue_fill(h, op.g, op.slot, st_lo, st_mid, flags, cp));
         break;
       case OP_FILL_B:
-        HIPCHK(h, issue_fill(h, op.g, op.slot, h->fill_split, lb, flags, cp));
+        HIPCHK(h, issue_fill(h, op.g, op.slot, st_mid, st_hi, flags, cp));
         HIPCHK(h, hipEventRecord(h->filled[op.slot], cp));
         break;
       case OP_WAIT_FILL:
@@ -647,14 +690,14 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         HIPCHK(h, time_end(h, cs));
         break;
       case OP_ATTN:
-        HIPCHK(h, run_attn_half(h, slot, (int)(op.g % c.num_layers), hidden, positions, block_tables,
-                                max_blocks_per_seq, batch, cs));
+        HIPCHK(h, run_attn_half(h, ffn_only ? own : slot, layer, hidden, positions, block_tables, max_blocks_per_seq,
+                                batch, cs));
         break;
       case OP_MID:
         HIPCHK(h, hipEventRecord(h->mid[op.slot], cs));
         break;
       case OP_PROJ:
-        HIPCHK(h, run_proj_half(h, slot, (int)(op.g % c.num_layers), hidden, batch, cs));
+        HIPCHK(h, run_proj_half(h, ffn_only ? own : slot, slot, layer, hidden, batch, cs));
         break;
       case OP_DONE:
         HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
@@ -665,8 +708,28 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
       case OP_WAIT_MID:
         HIPCHK(h, hipStreamWaitEvent(cp, h->mid[op.slot], 0));
         break;
+      case OP_LOCAL:
+        HIPCHK(h, run_layer(h, own, layer, hidden, positions, block_tables, max_blocks_per_seq, batch, cs));
+        break;
     }
   }
+  return SIDP_OK;
+}
+
+int sidp_set_pooling(sidp_handle* h, int32_t mode, int32_t ranks, int32_t rank) {
+  if (!h) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  if (mode != SIDP_POOL_LAYER && mode != SIDP_POOL_FFN) return SIDP_EINVAL;
+  if (ranks < 0 || (ranks > 0 && (rank < 0 || rank >= ranks))) return SIDP_EINVAL;
+  h->pool_mode = mode;
+  h->ranks = ranks;
+  h->rank = ranks > 0 ? rank : 0;
+  h->streamed_layers.clear();
+  for (int l = 0; l < h->cfg.num_layers; l++)
+    if (!layer_owned(l, h->ranks, h->rank)) h->streamed_layers.push_back(l);
+  // the slots no longer hold what the ring expects: restart it
+  h->ring_started = false;
+  h->ring_g = 0;
   return SIDP_OK;
 }
 
@@ -705,11 +768,13 @@ int sidp_timing_collect(sidp_handle* h, double* ms, int32_t* launches) {
   return SIDP_OK;
 }
 
-int sidp_plan(int32_t num_layers, int32_t steps, int32_t* ops_out, int32_t* n_ops) {
+int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, int32_t* ops_out, int32_t* n_ops) {
   if (num_layers < 1 || steps < 0 || !n_ops) return SIDP_EINVAL;
+  if (ranks < 0 || (ranks > 0 && (rank < 0 || rank >= ranks))) return SIDP_EINVAL;
   std::vector<RingOp> ops;
-  if (steps > 0) ring_prologue(0, ops);
-  for (int64_t g = 0; g < (int64_t)num_layers * steps; g++) ring_layer(g, g == 0, ops);
+  int64_t ring_g = 0;
+  bool started = false;
+  for (int t = 0; t < steps; t++) build_step(num_layers, ranks, rank, t, &ring_g, &started, ops);
   if ((int64_t)ops.size() > *n_ops) return SIDP_EINVAL;
   if (!ops.empty() && !ops_out) return SIDP_EINVAL;
   for (size_t i = 0; i < ops.size(); i++) {

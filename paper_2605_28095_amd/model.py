@@ -15,6 +15,7 @@ from . import (
     sidp_layer_bytes,
     sidp_pool_init,
     sidp_pool_load_layer,
+    sidp_set_pooling,
     sidp_sync,
 )
 
@@ -63,6 +64,11 @@ class WaSDecoder:
 
     def load_layer(self, layer, weights, stream=None):
         sidp_pool_load_layer(self.h, layer, weights, stream)
+
+    def set_pooling(self, mode, ranks=0, rank=0):
+        """What a streamed layer stages (SIDP_POOL_LAYER / SIDP_POOL_FFN) and which
+        layers this rank owns (l % ranks == rank); call between steps, after sync."""
+        sidp_set_pooling(self.h, mode, ranks, rank)
 
     def step(self, hidden, positions, block_tables, flags=SIDP_STREAMED, compute=None, copy=None):
         compute = compute if compute is not None else torch.cuda.current_stream(self.device)

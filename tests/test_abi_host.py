@@ -67,10 +67,18 @@ def test_kv_alloc_errors():
     assert sidp.sidp_kv_alloc([], 1, 16, 0, 0, 1) == []
 
 
-@pytest.mark.parametrize("L,steps", [(1, 1), (3, 2), (80, 3), (8, 0)])
-def test_plan_matches_oracle_schedule(L, steps):
+@pytest.mark.parametrize("L,steps,ranks,rank", [(1, 1, 0, 0), (3, 2, 0, 0), (80, 3, 0, 0), (8, 0, 0, 0),
+                                               (7, 3, 3, 1), (80, 2, 8, 0), (4, 2, 1, 0), (5, 2, 2, 1), (3, 1, 9, 8)])
+def test_plan_matches_oracle_schedule(L, steps, ranks, rank):
     import paper_2605_28095_amd as sidp
-    assert sidp.sidp_plan(L, steps) == oracle.was_schedule(L, steps)
+    assert sidp.sidp_plan(L, steps, ranks, rank) == oracle.was_schedule(L, steps, ranks, rank)
+
+
+def test_plan_and_pooling_reject_bad_ranks():
+    import paper_2605_28095_amd as sidp
+    for ranks, rank in [(-1, 0), (2, 2), (3, -1)]:
+        assert sidp.raw_call("sidp_plan", 4, 1, ranks, rank, None, None) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_set_pooling", None, 0, 0, 0) == sidp.SIDP_EINVAL
 
 
 def test_config_validation_on_host():
@@ -99,4 +107,4 @@ def test_null_handle_calls_are_rejected():
     assert sidp.raw_call("sidp_sync", None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_destroy", None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_decode_step", None, None, None, None, 1, 1, 0, None, None) == sidp.SIDP_EINVAL
-    assert sidp.raw_call("sidp_plan", 0, 1, None, None) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_plan", 0, 1, 0, 0, None, None) == sidp.SIDP_EINVAL

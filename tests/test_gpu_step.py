@@ -115,6 +115,54 @@ def test_streamed_equals_resident_bitexact(lib):
         st.close()
 
 
+@pytest.mark.parametrize("mode,ranks,rank", [("ffn", 0, 0), ("layer", 2, 1), ("ffn", 3, 0), ("layer", 1, 0),
+                                              ("ffn", 4, 3)])
+def test_pooling_streamed_equals_resident_bitexact(lib, mode, ranks, rank):
+    """FFN-only staging and owned layers (computed from the pool, no slot) give
+    the resident bits over three steps, with every slot poisoned and each fill
+    delayed, so a missing wait or a wrong weight source shows up."""
+    cfg = _small_stack_cfg(num_layers=5)
+    st = Stack(cfg, gains="random", regions=2, reserve=3)
+    try:
+        copy = torch.cuda.Stream()
+        outs = {}
+        pool_mode = lib.SIDP_POOL_FFN if mode == "ffn" else lib.SIDP_POOL_LAYER
+        for name, flags in [("resident", lib.SIDP_RESIDENT),
+                            ("streamed", lib.SIDP_STREAMED | lib.SIDP_DEBUG_POISON | lib.SIDP_DEBUG_DELAY)]:
+            st.reset()
+            if name == "streamed":
+                st.dec.set_pooling(pool_mode, ranks, rank)
+            for s in range(3):
+                st.dec.step(st.hidden, st.positions + s, st.bt, flags, copy=copy)
+            st.dec.sync()
+            outs[name] = (st.hidden.cpu().numpy().copy(), bits(st.dec.k_cache), bits(st.dec.v_cache))
+        ref, got = outs["resident"], outs["streamed"]
+        assert np.all(np.isfinite(ref[0]))
+        assert np.array_equal(got[0].view(np.uint32), ref[0].view(np.uint32))
+        assert np.array_equal(got[1], ref[1]) and np.array_equal(got[2], ref[2])
+        # back to whole-layer staging with no owned layers: still the same bits
+        st.reset()
+        st.dec.set_pooling(lib.SIDP_POOL_LAYER, 0, 0)
+        for s in range(3):
+            st.dec.step(st.hidden, st.positions + s, st.bt, lib.SIDP_STREAMED, copy=copy)
+        st.dec.sync()
+        assert np.array_equal(st.hidden.cpu().numpy().view(np.uint32), ref[0].view(np.uint32))
+    finally:
+        st.close()
+
+
+def test_set_pooling_rejects_bad_arguments(lib):
+    cfg = _small_stack_cfg(num_layers=2)
+    st = Stack(cfg, gains="one")
+    try:
+        for mode, ranks, rank in [(2, 0, 0), (0, -1, 0), (0, 2, 2), (1, 3, -1)]:
+            with pytest.raises(lib.SidpError) as e:
+                st.dec.set_pooling(mode, ranks, rank)
+            assert e.value.code == lib.SIDP_EINVAL
+    finally:
+        st.close()
+
+
 def test_zero_projections_keep_residual_bitexact(lib):
     """W_o = W_down = 0: the fp32 residual stream passes every layer unchanged."""
     cfg = _small_stack_cfg(num_layers=3)

@@ -16,7 +16,7 @@ import torch.nn.functional as F
 import oracle
 from oracle import decode as od
 from oracle import kvalloc as ka
-from oracle.schedule import was_schedule
+from oracle.schedule import was_schedule, streamed_layer
 import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -245,6 +245,32 @@ def test_was_schedule_ordering():
     # fills are issued for every layer, plus one ahead into the next iteration
     assert [g for (k, g, s) in ops if k == "fill_a"] == list(range(total + 1))
     assert was_schedule(L, 0) == []
+
+
+def test_was_schedule_with_owned_layers():
+    """With d pooling ranks, rank r computes the layers it owns (l mod d = r)
+    straight from its pool and streams the rest through the ring: owned
+    layers get no read and no slot, every other layer keeps the properties
+    above, and layer order is kept."""
+    L, steps, d, r = 7, 3, 3, 1
+    ops = was_schedule(L, steps, d, r)
+    assert was_schedule(L, steps) == was_schedule(L, steps, 0, 0)
+    streamed = [l for l in range(L) if l % d != r]
+    local = [n for (k, n, s) in ops if k == "local"]
+    assert local == [t * L + l for t in range(steps) for l in range(L) if l % d == r]
+    ring_only = [op for op in ops if op[0] != "local"]
+    assert ring_only == was_schedule(len(streamed), steps)  # the ring sees the non-owned layers only
+    # compute happens in layer order: each step's layers appear as l = 0 .. L-1
+    order = []
+    for k, n, s in ops:
+        if k == "local":
+            order.append(n % L)
+        elif k == "attn":
+            order.append(streamed_layer(n, L, d, r))
+    assert order == [l for _ in range(steps) for l in range(L)]
+    # owning every layer (d = 1) leaves no ring at all; owning none is the plain ring
+    assert all(k == "local" for (k, n, s) in was_schedule(4, 2, 1, 0))
+    assert was_schedule(4, 2, 5, 4) == was_schedule(4, 2)  # rank 4 of 5 owns none of 4 layers
 
 
 # ---------------------------------------------------------------- whole layer
