@@ -128,6 +128,37 @@ def cpu_baseline(cfg, weights_for_layer, kv_rows, x_rows, pos_rows, tabs_rows, n
     return rows / (per_layer * cfg["num_layers"]), threads, dt
 
 
+def cas_leg(dec, cfg, replicas, rows, stream, reps=20):
+    """Owner-side Compute-as-a-Service on layer 0: the FFN over `replicas`
+    replicas' rows fused into one call, against one call per replica."""
+    import torch
+    import paper_2605_28095_amd as sidp
+    H = cfg["hidden"]
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev).manual_seed(7)
+    xs = [(0.5 * torch.randn(rows, H, device=dev, generator=g)).to(torch.bfloat16) for _ in range(replicas)]
+    ys = [torch.empty(rows, H, device=dev, dtype=torch.float32) for _ in range(replicas)]
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    fused = timed(lambda: sidp.sidp_cas_ffn(dec.h, 0, xs, [rows] * replicas, ys, stream))
+    separate = timed(lambda: [sidp.sidp_cas_ffn(dec.h, 0, [x], [rows], [y], stream) for x, y in zip(xs, ys)])
+    dec.sync()
+    log(f"CaS FFN, {replicas} x {rows} rows: fused {fused:.3f} ms, one call per replica {separate:.3f} ms")
+    return {"replicas": replicas, "rows_per_replica": rows, "layer": 0, "fused_ms": round(fused, 4),
+            "per_replica_ms": round(separate, 4), "fusion_speedup": round(separate / fused, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +172,9 @@ def main():
                     help="stage whole layers, or only their FFN part (attention weights read in place)")
     ap.add_argument("--ranks", type=int, default=0, help="pooling ranks d: layers l with l %% d == rank are owned")
     ap.add_argument("--rank", type=int, default=0)
+    ap.add_argument("--cas", type=int, default=0,
+                    help="also time the owner-side CaS FFN over this many replicas (0: skip)")
+    ap.add_argument("--cas-rows", type=int, default=16, help="rows per CaS replica")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -309,6 +343,8 @@ def main():
                          f"float64 with bf16 storage rounding; {dt:.1f}s; tok/s = rows / (s per layer x {L})"}
         log(f"oracle baseline: {val:.3f} tok/s over {dt:.1f}s with {threads} BLAS threads")
 
+    cas = cas_leg(dec, cfg, args.cas, args.cas_rows, compute) if args.cas > 0 else None
+
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
@@ -326,6 +362,8 @@ def main():
         "resident_ms_per_step": round(resident_ms, 3) if resident_ms else None,
         "fill_stall_ms_per_step": kernels["wait_fill"]["ms_per_step"] if "wait_fill" in kernels else None,
     }
+    if cas:
+        out["cas"] = cas
     print(json.dumps(out), flush=True)
     dec.close()
 

@@ -217,6 +217,31 @@ int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
 #define SIDP_POOL_FFN   1
 int sidp_set_pooling(sidp_handle *h, int32_t mode, int32_t ranks, int32_t rank);
 
+/* ---- Compute-as-a-Service, owner side ----
+ * §4.3: in the small-batch tail, non-owner replicas send their FFN inputs to
+ * the layer's owner, which concatenates them with its own rows in a staging
+ * buffer, runs the FFN once over all of them, splits the output along the same
+ * row boundaries and returns each slice; replicas running dummy iterations
+ * send nothing and get no compute. This handle is the owner: it computes
+ * layer `layer`'s FFN from its pool (the layer must be loaded).
+ *   x_in[r]  device, bf16 [rows[r], hidden] row-major, 16-byte aligned:
+ *            replica r's FFN input (the RMSNorm output before the FFN).
+ *   rows[r]  host; 0 marks a dummy replica: x_in[r], y_out[r] are not touched.
+ *   y_out[r] device, fp32 [rows[r], hidden], 16-byte aligned: receives
+ *            down(silu(x Wg^T) * (x Wu^T)), the FFN output without the
+ *            residual, which the replica adds to its residual stream (as
+ *            the streamed step's down projection does).
+ * Rows are processed in replica order; sum of rows <= max_batch and
+ * n_replicas <= SIDP_CAS_MAX_REPLICAS, else SIDP_EINVAL. On one GPU the
+ * transfers into the staging buffer and back are device copies. The math is
+ * the decode step's FFN; the fused projections split K by the total row
+ * count, so a row's output can differ from a per-replica run in fp32
+ * summation order only. Uses the handle's activation buffers: do not overlap
+ * with a decode step on the same handle. */
+#define SIDP_CAS_MAX_REPLICAS 16
+int sidp_cas_ffn(sidp_handle *h, int32_t layer, int32_t n_replicas, const void *const *x_in, const int32_t *rows,
+                 void *const *y_out, void *stream);
+
 /* ---- the slot-ring plan (host only) ----
  * The order in which sidp_decode_step issues its operations on the two
  * streams, for `steps` streamed calls of num_layers layers with 2 slots, on

@@ -45,6 +45,8 @@ from .decode import (  # noqa: F401
     silu,
     linear,
     swiglu,
+    ffn,
+    cas_ffn,
     paged_gqa_attention,
     decode_layer,
     decode_stack,

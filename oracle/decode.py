@@ -92,6 +92,35 @@ def swiglu(h, w_gate, w_up):
     return silu(linear(h, w_gate)) * linear(h, w_up)
 
 
+def ffn(h, w_gate, w_up, w_down, round_bf16=False):
+    """The FFN of a decoder layer on already normed rows h: down(SwiGLU(h)),
+    with the SwiGLU output rounded to bf16 where a bf16 model stores it."""
+    a = swiglu(h, w_gate, w_up)
+    if round_bf16:
+        a = round_to_bf16(a)
+    return linear(a, w_down)
+
+
+def cas_ffn(inputs, w_gate, w_up, w_down, round_bf16=False):
+    """Compute-as-a-Service at a layer's owner (§4.3): the rows of all replicas
+    that are not running a dummy iteration are stacked into one batch, the
+    FFN runs once over it, and the output is cut back at the same row
+    boundaries. inputs: per replica an (rows, H) array, or None for a dummy
+    replica. Returns the per-replica outputs (None for dummies)."""
+    live = [x for x in inputs if x is not None and len(x) > 0]
+    if not live:
+        return [None for _ in inputs]
+    y = ffn(np.concatenate(live, axis=0), w_gate, w_up, w_down, round_bf16)
+    out, o = [], 0
+    for x in inputs:
+        if x is None or len(x) == 0:
+            out.append(None)
+            continue
+        out.append(y[o:o + len(x)])
+        o += len(x)
+    return out
+
+
 def paged_gqa_attention(q, k_cache, v_cache, block_table, seq_len, block_size):
     """Decode attention of one sequence over its paged KV.
 

@@ -48,8 +48,10 @@ EXPORTED = [
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
-    "sidp_timing_collect", "sidp_set_pooling",
+    "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn",
 ]
+
+SIDP_CAS_MAX_REPLICAS = 16
 
 
 class SidpError(RuntimeError):
@@ -99,6 +101,7 @@ _sigs = {
     "sidp_sync": (ctypes.c_int, [_P]),
     "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
     "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
+    "sidp_cas_ffn": (ctypes.c_int, [_P, _I, _I, ctypes.POINTER(_P), _PI, ctypes.POINTER(_P), _P]),
     "sidp_rmsnorm": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I, _I, _P]),
     "sidp_packed_bytes": (_Z, [_I, _I]),
     "sidp_pack_linear": (ctypes.c_int, [_P, _I, _I, _P, _P]),
@@ -220,6 +223,16 @@ def sidp_plan(num_layers, steps, ranks=0, rank=0):
 
 def sidp_set_pooling(h, mode, ranks=0, rank=0):
     _check(_lib.sidp_set_pooling(h, mode, ranks, rank), "sidp_set_pooling")
+
+
+def sidp_cas_ffn(h, layer, xs, rows, ys, stream=None):
+    """Owner-side CaS FFN: xs[r] bf16 [rows[r], H] in, ys[r] fp32 [rows[r], H]
+    out; rows[r] == 0 marks a dummy replica (xs[r], ys[r] may be None)."""
+    n = len(rows)
+    xp = (_P * n)(*[_ptr(x) if x is not None else None for x in xs])
+    yp = (_P * n)(*[_ptr(y) if y is not None else None for y in ys])
+    rr = (ctypes.c_int32 * n)(*rows)
+    _check(_lib.sidp_cas_ffn(h, layer, n, xp, rr, yp, _stream(stream)), "sidp_cas_ffn")
 
 
 def sidp_rmsnorm(x, gain, eps, out, rows, n, stream=None):

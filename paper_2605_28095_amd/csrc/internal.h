@@ -97,6 +97,19 @@ hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s);
 hipError_t launch_attention(const AttnCall& c, hipStream_t s);
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);
+
+// Rows moved between per-replica buffers and one contiguous staging buffer:
+// staging row i belongs to replica r with row_off[r] <= i < row_off[r + 1].
+constexpr int kMaxReplicas = 16;
+struct RowMove {
+  void* rep[kMaxReplicas];
+  int row_off[kMaxReplicas + 1];
+  int n;             // replicas listed
+  size_t row_bytes;  // a multiple of 16
+  void* staging;
+  int gather;        // 1: replicas -> staging; 0: staging -> replicas
+};
+hipError_t launch_rows_move(const RowMove& m, hipStream_t s);
 hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s);
 hipError_t launch_poison(void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_spin(int64_t cycles, hipStream_t s);

@@ -87,6 +87,27 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipSt
   return hipGetLastError();
 }
 
+// One workgroup per staging row; 16-byte copies.
+__global__ void __launch_bounds__(256) k_rows_move(RowMove m) {
+  const int i = blockIdx.x;
+  int r = 0;
+  while (r + 1 < m.n && m.row_off[r + 1] <= i) r++;
+  uint8_t* srow = (uint8_t*)m.staging + (size_t)i * m.row_bytes;
+  uint8_t* rrow = (uint8_t*)m.rep[r] + (size_t)(i - m.row_off[r]) * m.row_bytes;
+  const uint8_t* from = m.gather ? rrow : srow;
+  uint8_t* to = m.gather ? srow : rrow;
+  for (size_t j = (size_t)threadIdx.x * 16; j < m.row_bytes; j += 256 * 16)
+    *(u32x4_t*)(to + j) = *(const u32x4_t*)(from + j);
+}
+
+hipError_t launch_rows_move(const RowMove& m, hipStream_t s) {
+  if (m.n < 1 || m.n > kMaxReplicas || m.row_bytes % 16) return hipErrorInvalidValue;
+  const int rows = m.row_off[m.n];
+  if (rows <= 0) return hipSuccess;
+  k_rows_move<<<rows, 256, 0, s>>>(m);
+  return hipGetLastError();
+}
+
 __global__ void k_poison(uint32_t* __restrict__ dst, size_t n) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = 0xffffffffu;

@@ -266,7 +266,7 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
             if (a.bias) v += bf2f(a.bias[n]);
             ((uint16_t*)a.out)[o] = f2bf(v);
           } else {
-            ((float*)a.out)[o] = a.resid[o] + acc[m][nf][r];
+            ((float*)a.out)[o] = a.resid ? a.resid[o] + acc[m][nf][r] : acc[m][nf][r];
           }
         }
       }
@@ -299,7 +299,7 @@ __global__ void k_splitk_reduce(GemmArgs a) {
       if (a.bias) v += bf2f(a.bias[c]);
       ((uint16_t*)a.out)[idx] = f2bf(v);
     } else {
-      ((float*)a.out)[idx] = a.resid[idx] + v;
+      ((float*)a.out)[idx] = a.resid ? a.resid[idx] + v : v;
     }
   }
 }

@@ -172,6 +172,7 @@ struct sidp_handle {
   // H = 8192), kept resident beside the pool so that layer l's down-projection
   // reduction can apply layer l + 1's norm before layer l + 1's slot is read.
   uint16_t* g_attn_all = nullptr;
+  float* cas_y = nullptr;  // owner-side FFN output of the concatenated CaS rows [max_batch][H] fp32
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
@@ -229,7 +230,7 @@ size_t sidp_layer_bytes(const sidp_config* cfg) {
 }
 
 static void free_device(sidp_handle* h) {
-  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->g_attn_all, h->rope_cos, h->rope_sin, h->err};
+  void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->g_attn_all, h->cas_y, h->rope_cos, h->rope_sin, h->err};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; i++) {
@@ -290,6 +291,7 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
       {(void**)&h->attn_part, std::max<size_t>(part_bytes, 256)},
       {(void**)&h->attn_plan, attn_plan_bytes(c.max_batch, h->attn_max_parts)},
       {(void**)&h->g_attn_all, (size_t)c.num_layers * H * 2},
+      {(void**)&h->cas_y, B * H * 4},
       {(void**)&h->rope_cos, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->rope_sin, (size_t)c.max_seq_len * (D / 2) * 4},
       {(void**)&h->err, 256},
@@ -713,6 +715,50 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         break;
     }
   }
+  return SIDP_OK;
+}
+
+static_assert(SIDP_CAS_MAX_REPLICAS == kMaxReplicas, "replica table size");
+
+int sidp_cas_ffn(sidp_handle* h, int32_t layer, int32_t n_replicas, const void* const* x_in, const int32_t* rows,
+                 void* const* y_out, void* stream) {
+  if (!h || !x_in || !rows || !y_out || n_replicas < 1 || n_replicas > SIDP_CAS_MAX_REPLICAS) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  const sidp_config& c = h->cfg;
+  if (layer < 0 || layer >= c.num_layers) return SIDP_EINVAL;
+  if (!h->pool || !h->loaded[layer]) return SIDP_ESTATE;
+  const int H = c.hidden;
+  RowMove in{}, out{};
+  int total = 0, n = 0;
+  for (int r = 0; r < n_replicas; r++) {
+    if (rows[r] < 0) return SIDP_EINVAL;
+    if (rows[r] == 0) continue;  // a dummy replica: nothing moved, nothing computed
+    if (!x_in[r] || !y_out[r] || ((uintptr_t)x_in[r] % 16) || ((uintptr_t)y_out[r] % 16)) return SIDP_EINVAL;
+    if (total + rows[r] > c.max_batch) return SIDP_EINVAL;
+    in.rep[n] = const_cast<void*>(x_in[r]);
+    out.rep[n] = y_out[r];
+    in.row_off[n] = out.row_off[n] = total;
+    total += rows[r];
+    n++;
+  }
+  if (total == 0) return SIDP_OK;
+  in.row_off[n] = out.row_off[n] = total;
+  in.n = out.n = n;
+  in.row_bytes = (size_t)H * 2;
+  out.row_bytes = (size_t)H * 4;
+  in.staging = h->h;
+  out.staging = h->cas_y;
+  in.gather = 1;
+  out.gather = 0;
+  hipStream_t s = (hipStream_t)stream;
+  const uint8_t* wb = h->pool + (size_t)layer * h->blob.total;
+  HIPCHK(h, launch_rows_move(in, s));
+  HIPCHK(h, launch_linear(linear_call(h, h->h, total, H, wb + h->blob.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr,
+                                      nullptr, h->act), s));
+  HIPCHK(h, launch_linear(linear_call(h, h->act, total, c.ffn_dim, wb + h->blob.w_d, H, SIDP_EPI_RESID, nullptr,
+                                      nullptr, h->cas_y), s));
+  HIPCHK(h, launch_rows_move(out, s));
+  h->last_compute = s;
   return SIDP_OK;
 }
 

@@ -214,6 +214,42 @@ def test_slot_mapping_brute_force():
     assert len(slots) == sum(c + 1 for c in ctx)
 
 
+def test_ffn_matches_transformers_mlp():
+    """The oracle's FFN against transformers' LlamaMLP (SiLU-gated) in float64."""
+    from transformers import LlamaConfig
+    from transformers.models.llama.modeling_llama import LlamaMLP
+    H, F = 48, 80
+    g = torch.Generator().manual_seed(5)
+    hc = LlamaConfig(hidden_size=H, intermediate_size=F, hidden_act="silu", num_attention_heads=4,
+                     num_key_value_heads=4)
+    mlp = LlamaMLP(hc).to(torch.float64)
+    with torch.no_grad():
+        for lin in (mlp.gate_proj, mlp.up_proj, mlp.down_proj):
+            lin.weight.copy_(torch.randn(lin.weight.shape, generator=g, dtype=torch.float64) * 0.1)
+        x = torch.randn(7, H, generator=g, dtype=torch.float64)
+        want = mlp(x).numpy()
+    got = oracle.ffn(x.numpy(), mlp.gate_proj.weight.detach().numpy(), mlp.up_proj.weight.detach().numpy(),
+                     mlp.down_proj.weight.detach().numpy())
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
+def test_cas_ffn_is_per_replica_ffn():
+    """CaS fuses the replicas' rows into one FFN call and cuts the output back:
+    every live replica gets exactly its own rows' FFN, in order, and dummy
+    replicas get nothing (§4.3, numerically equivalent to computing locally)."""
+    rng = np.random.default_rng(2)
+    H, F = 16, 24
+    wg, wu, wd = rng.normal(size=(F, H)), rng.normal(size=(F, H)), rng.normal(size=(H, F))
+    xs = [rng.normal(size=(3, H)), None, rng.normal(size=(1, H)), np.zeros((0, H)), rng.normal(size=(5, H))]
+    ys = oracle.cas_ffn(xs, wg, wu, wd)
+    assert ys[1] is None and ys[3] is None
+    for x, y in zip(xs, ys):
+        if y is not None:
+            assert y.shape == x.shape
+            np.testing.assert_allclose(y, oracle.ffn(x, wg, wu, wd), rtol=1e-13, atol=1e-12)
+    assert oracle.cas_ffn([None, None], wg, wu, wd) == [None, None]
+
+
 # ---------------------------------------------------------------- schedule
 
 def test_was_schedule_ordering():
