@@ -30,7 +30,7 @@ namespace {
 constexpr int kSlots = 2;
 constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
-constexpr int kFillPartAPercent = 35;  // share of a layer's fill issued before its predecessor's attention
+constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
