@@ -110,7 +110,9 @@ struct RowMove {
   int gather;        // 1: replicas -> staging; 0: staging -> replicas
 };
 hipError_t launch_rows_move(const RowMove& m, hipStream_t s);
-hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s);
+// loads: 16-byte loads in flight per lane (2, 4 or 8): how hard the fill
+// presses on HBM while it shares the chip with the layer kernels
+hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, int loads, hipStream_t s);
 hipError_t launch_poison(void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_spin(int64_t cycles, hipStream_t s);
 

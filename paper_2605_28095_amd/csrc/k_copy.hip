@@ -5,6 +5,8 @@
 // copy on the CUs; a copy kernel of our own lets the runtime choose how many
 // workgroups (CUs) the fill may occupy while compute runs beside it.
 // Also: a NaN poison fill and a bounded spin, used to expose missing waits.
+#include <cstdlib>
+
 #include "common.h"
 #include "internal.h"
 
@@ -29,47 +31,82 @@ __global__ void __launch_bounds__(256) k_copy16(const f4v_t* __restrict__ src, f
 }
 
 // Background slot fill: runs beside the layer kernels instead of ahead of
-// them. One 4-wave workgroup per CU, at most 16 VGPRs per wave, scalar buffer
-// bases: a fill wave fits in the registers a projection or attention SIMD
-// leaves free (2 x 248 + 16 = 512). The 81 KB of LDS it requests and never
-// touches keeps two fill workgroups off one CU (2 x 81 KB > 160 KB) while one
-// still fits beside two projection (2 x 32 KB) or two attention (2 x 36 KB)
-// workgroups, so the fill never claims the resources a layer kernel needs.
+// them. One 4-wave workgroup per CU with few VGPRs per wave and scalar buffer
+// bases, so a fill wave fits in the registers a projection or attention SIMD
+// leaves free (those kernels use at most 232 of a lane's 512 registers with
+// two waves per SIMD). The 81 KB of LDS it requests and never touches keeps
+// two fill workgroups off one CU (2 x 81 KB > 160 KB) while one still fits
+// beside two projection (2 x 32 KB) or two attention (2 x 34 KB) workgroups,
+// so the fill never claims the resources a layer kernel needs. U 16-byte
+// loads per lane are in flight per iteration.
 constexpr int kFillLdsBytes = 81 * 1024;
 constexpr uint32_t kFillRsrcWord3 = 0x00020000u;
 
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(16)))
-k_fill_bg(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
-  extern __shared__ uint8_t fill_lds_reserve[];
+template <int U>
+__device__ __forceinline__ void fill_body(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(src), (short)0,
                                                                       (int)(n16 * 16u), (int)kFillRsrcWord3);
   const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(dst, (short)0, (int)(n16 * 16u),
                                                                       (int)kFillRsrcWord3);
   const uint32_t stride = gridDim.x * 256u;
   uint32_t i = blockIdx.x * 256u + threadIdx.x;
-  for (; i + stride < n16; i += 2 * stride) {
-    const f4v_t a = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16u, 0, 2));
-    const f4v_t b = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (i + stride) * 16u, 0, 2));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, a), rd, i * 16u, 0, 2);
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, b), rd, (i + stride) * 16u, 0, 2);
+  for (; i + (U - 1) * stride < n16; i += U * stride) {
+    u32x4_t v[U];
+#pragma unroll
+    for (int u = 0; u < U; u++)
+      v[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (i + u * stride) * 16u, 0, 2));
+#pragma unroll
+    for (int u = 0; u < U; u++) __builtin_amdgcn_raw_buffer_store_b128(v[u], rd, (i + u * stride) * 16u, 0, 2);
   }
-  if (i < n16) {
-    const f4v_t a = __builtin_bit_cast(f4v_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16u, 0, 2));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, a), rd, i * 16u, 0, 2);
+  for (; i < n16; i += stride) {
+    const u32x4_t a = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16u, 0, 2));
+    __builtin_amdgcn_raw_buffer_store_b128(a, rd, i * 16u, 0, 2);
   }
 }
 
-hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s) {
-  if (bytes == 0) return hipSuccess;
-  if (bytes % 16 || bytes >= ((size_t)1 << 31)) return launch_copy(src, dst, bytes, 0, s);
+// The register caps are literals (the attribute takes no expression).
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(16)))
+k_fill_bg2(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
+  extern __shared__ uint8_t fill_lds_reserve[];
+  fill_body<2>(src, dst, n16);
+}
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(24)))
+k_fill_bg4(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
+  extern __shared__ uint8_t fill_lds_reserve[];
+  fill_body<4>(src, dst, n16);
+}
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(40)))
+k_fill_bg8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
+  extern __shared__ uint8_t fill_lds_reserve[];
+  fill_body<8>(src, dst, n16);
+}
+
+template <int U>
+static hipError_t launch_fill_u(const void* src, void* dst, size_t bytes, int num_cus, hipStream_t s) {
+  const void* k = U == 8 ? (const void*)k_fill_bg8 : U == 4 ? (const void*)k_fill_bg4 : (const void*)k_fill_bg2;
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_fill_bg, hipFuncAttributeMaxDynamicSharedMemorySize, kFillLdsBytes);
+    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, kFillLdsBytes);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  k_fill_bg<<<num_cus, 256, kFillLdsBytes, s>>>((const uint8_t*)src, (uint8_t*)dst, (uint32_t)(bytes / 16));
+  const uint8_t* sp = (const uint8_t*)src;
+  uint8_t* dp = (uint8_t*)dst;
+  const uint32_t n16 = (uint32_t)(bytes / 16);
+  if (U == 8) k_fill_bg8<<<num_cus, 256, kFillLdsBytes, s>>>(sp, dp, n16);
+  else if (U == 4) k_fill_bg4<<<num_cus, 256, kFillLdsBytes, s>>>(sp, dp, n16);
+  else k_fill_bg2<<<num_cus, 256, kFillLdsBytes, s>>>(sp, dp, n16);
   return hipGetLastError();
+}
+
+hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, int loads, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if (bytes % 16 || bytes >= ((size_t)1 << 31)) return launch_copy(src, dst, bytes, 0, s);
+  switch (loads) {
+    case 8: return launch_fill_u<8>(src, dst, bytes, num_cus, s);
+    case 4: return launch_fill_u<4>(src, dst, bytes, num_cus, s);
+    default: return launch_fill_u<2>(src, dst, bytes, num_cus, s);
+  }
 }
 
 __global__ void k_copy_tail(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, size_t n) {

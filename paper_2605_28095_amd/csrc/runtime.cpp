@@ -177,6 +177,9 @@ struct sidp_handle {
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
   int fill_pct = 0;       // percent of the staged range in fill part A
+  // loads in flight per lane of the background fill: part A overlaps attention and may press harder;
+  // part B runs beside the projections, which lose more than the fill gains when it presses harder
+  int fill_loads_a = 4, fill_loads_b = 2;
   // pooling: which part of a layer is staged, and which layers this rank owns
   int pool_mode = SIDP_POOL_LAYER;
   int ranks = 0, rank = 0;          // layer l is owned (never staged) when ranks > 0 and l % ranks == rank
@@ -317,6 +320,8 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   }
   h->fill_pct = kFillPartAPercent;
   if (const char* e = std::getenv("SIDP_FILL_SPLIT")) h->fill_pct = std::min(100, std::max(0, std::atoi(e)));
+  if (const char* e = std::getenv("SIDP_FILL_LOADS_A")) h->fill_loads_a = std::atoi(e);
+  if (const char* e = std::getenv("SIDP_FILL_LOADS_B")) h->fill_loads_b = std::atoi(e);
   for (int l = 0; l < c.num_layers; l++) h->streamed_layers.push_back(l);
   *out = h;
   return SIDP_OK;
@@ -624,7 +629,7 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
-  else e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, cp);
+  else e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? h->fill_loads_a : h->fill_loads_b, cp);
   if (e != hipSuccess) return e;
   return time_end(h, cp);
 }
