@@ -159,6 +159,56 @@ def cas_leg(dec, cfg, replicas, rows, stream, reps=20):
             "per_replica_ms": round(separate, 4), "fusion_speedup": round(separate / fused, 3)}
 
 
+# MI355X xGMI: 7 links of about 153 GB/s per direction; a rank pulling from its
+# d - 1 = 7 owners at once (peak-shifted) sees at most all of them.
+XGMI_LINK_GBS = 153.0
+XGMI_LINKS = 7
+
+
+def bth_leg(dec, hidden, pos, bt, stage_bytes, L, batches, stream, reps=3):
+    """§4.3 profile: per-layer forward time T(B) from resident steps on the
+    first B rows, against the time to fetch one layer's staged weights (the
+    emulated same-HBM copy, measured; one and seven xGMI links, modeled).
+    B_th is the smallest profiled B with T(B) >= the fetch time."""
+    import torch
+    import paper_2605_28095_amd as sidp
+    layer_ms = []
+    for b in batches:
+        h = hidden[:b].clone()
+        for _ in range(2):
+            dec.step(h, pos[:b], bt[:b], sidp.SIDP_RESIDENT, compute=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            dec.step(h, pos[:b], bt[:b], sidp.SIDP_RESIDENT, compute=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        layer_ms.append(e0.elapsed_time(e1) / reps / L)
+    # the emulated fetch alone: one layer's staged bytes, pool -> slot, whole chip
+    src = torch.empty(stage_bytes, dtype=torch.uint8, device=hidden.device)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        sidp.sidp_copy(src, dst, stage_bytes, 0, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(5):
+        sidp.sidp_copy(src, dst, stage_bytes, 0, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fetch = {"same_hbm_copy": e0.elapsed_time(e1) / 5,
+             "xgmi_7_links_modeled": stage_bytes / (XGMI_LINKS * XGMI_LINK_GBS * 1e9) * 1e3,
+             "xgmi_1_link_modeled": stage_bytes / (XGMI_LINK_GBS * 1e9) * 1e3}
+    del src, dst
+    bth = {k: next((b for b, t in zip(batches, layer_ms) if t >= f), None) for k, f in fetch.items()}
+    log("B_th profile: " + ", ".join(f"B={b}: {t:.3f} ms/layer" for b, t in zip(batches, layer_ms)))
+    log("fetch per layer: " + ", ".join(f"{k} {v:.3f} ms" for k, v in fetch.items()) + f"; B_th {bth}")
+    return {"batches": batches, "layer_ms": [round(t, 4) for t in layer_ms],
+            "fetch_ms": {k: round(v, 4) for k, v in fetch.items()}, "staged_bytes": stage_bytes, "b_th": bth,
+            "note": "B_th = smallest profiled batch whose resident per-layer time covers the fetch; null: none"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -175,6 +225,8 @@ def main():
     ap.add_argument("--cas", type=int, default=0,
                     help="also time the owner-side CaS FFN over this many replicas (0: skip)")
     ap.add_argument("--cas-rows", type=int, default=16, help="rows per CaS replica")
+    ap.add_argument("--bth", action="store_true",
+                    help="also profile B_th: the smallest batch whose layer time covers one layer's weight fetch")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -344,6 +396,10 @@ def main():
         log(f"oracle baseline: {val:.3f} tok/s over {dt:.1f}s with {threads} BLAS threads")
 
     cas = cas_leg(dec, cfg, args.cas, args.cas_rows, compute) if args.cas > 0 else None
+    bth = None
+    if args.bth:
+        batches = [b for b in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512) if b <= B]
+        bth = bth_leg(dec, hidden, pos, bt, fill_bytes, L, batches, compute)
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
@@ -364,6 +420,8 @@ def main():
     }
     if cas:
         out["cas"] = cas
+    if bth:
+        out["bth"] = bth
     print(json.dumps(out), flush=True)
     dec.close()
 
