@@ -199,6 +199,11 @@ int sidp_sync(sidp_handle *h);
  * (launches[SIDP_NUM_KCLASSES], host); then recycles the events. Each pair
  * brackets one layer's launches of that class on the stream they run on. */
 int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
+/* Which kernel classes SIDP_TIMING brackets: bit i selects class i
+ * (SIDP_K_*); all by default. Each pair of events is a packet on the stream,
+ * so a caller timing one class leaves the others unbracketed. SIDP_EINVAL for
+ * bits past SIDP_NUM_KCLASSES. */
+int sidp_timing_select(sidp_handle *h, uint32_t class_mask);
 
 /* ---- pooling ----
  * What the weight cache stages, and which layers this rank owns (§4.1: each

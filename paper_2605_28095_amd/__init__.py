@@ -48,7 +48,7 @@ EXPORTED = [
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
-    "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn",
+    "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select",
 ]
 
 SIDP_CAS_MAX_REPLICAS = 16
@@ -102,6 +102,7 @@ _sigs = {
     "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
     "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
     "sidp_cas_ffn": (ctypes.c_int, [_P, _I, _I, ctypes.POINTER(_P), _PI, ctypes.POINTER(_P), _P]),
+    "sidp_timing_select": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "sidp_rmsnorm": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I, _I, _P]),
     "sidp_packed_bytes": (_Z, [_I, _I]),
     "sidp_pack_linear": (ctypes.c_int, [_P, _I, _I, _P, _P]),
@@ -275,6 +276,14 @@ def sidp_attention(h, q, region, positions, block_tables, max_blocks_per_seq, ba
 
 def sidp_copy(src, dst, nbytes, grid=0, stream=None):
     _check(_lib.sidp_copy(_ptr(src), _ptr(dst), nbytes, grid, _stream(stream)), "sidp_copy")
+
+
+def sidp_timing_select(h, classes):
+    """Bracket only the named kernel classes (names from KERNEL_CLASSES) under SIDP_TIMING."""
+    mask = 0
+    for c in classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    _check(_lib.sidp_timing_select(h, mask), "sidp_timing_select")
 
 
 def sidp_timing_collect(h):

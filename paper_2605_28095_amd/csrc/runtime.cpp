@@ -199,6 +199,7 @@ struct sidp_handle {
   std::vector<hipEvent_t> event_pool;
   std::vector<TimedPair> timed;
   bool timing = false;
+  uint32_t timing_mask = (1u << SIDP_NUM_KCLASSES) - 1;  // classes SIDP_TIMING brackets
 };
 
 #define HIPCHK(h, expr)                \
@@ -470,8 +471,10 @@ static LinearCall linear_call(const sidp_handle* h, const void* x, int m, int k,
 }
 
 // SIDP_TIMING: open a timed interval of kernel class `cls` on stream s.
+static bool timed_class(const sidp_handle* h, int cls) { return h->timing && ((h->timing_mask >> cls) & 1u); }
+
 static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
-  if (!h->timing) return hipSuccess;
+  if (!timed_class(h, cls)) return hipSuccess;
   hipEvent_t ev[2];
   for (int i = 0; i < 2; i++) {
     if (!h->event_pool.empty()) {
@@ -485,8 +488,8 @@ static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
   h->timed.push_back({cls, ev[0], ev[1]});
   return hipEventRecord(ev[0], s);
 }
-static hipError_t time_end(sidp_handle* h, hipStream_t s) {
-  if (!h->timing) return hipSuccess;
+static hipError_t time_end(sidp_handle* h, int cls, hipStream_t s) {
+  if (!timed_class(h, cls)) return hipSuccess;
   return hipEventRecord(h->timed.back().b, s);
 }
 
@@ -495,7 +498,7 @@ static hipError_t time_end(sidp_handle* h, hipStream_t s) {
     hipError_t te_;                                                 \
     if ((te_ = time_begin((h), (cls), (s))) != hipSuccess) return te_; \
     if ((te_ = (expr)) != hipSuccess) return te_;                   \
-    if ((te_ = time_end((h), (s))) != hipSuccess) return te_;       \
+    if ((te_ = time_end((h), (cls), (s))) != hipSuccess) return te_; \
   } while (0)
 
 // The attention half of a layer (norm, QKV, QK-norm/RoPE/KV append,
@@ -631,7 +634,7 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
   else e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? h->fill_loads_a : h->fill_loads_b, cp);
   if (e != hipSuccess) return e;
-  return time_end(h, cp);
+  return time_end(h, SIDP_K_FILL, cp);
 }
 
 int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, const int32_t* block_tables,
@@ -694,7 +697,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         // under SIDP_TIMING the interval around the wait is the compute stall on the fill
         HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
         HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
-        HIPCHK(h, time_end(h, cs));
+        HIPCHK(h, time_end(h, SIDP_K_WAIT_FILL, cs));
         break;
       case OP_ATTN:
         HIPCHK(h, run_attn_half(h, ffn_only ? own : slot, layer, hidden, positions, block_tables, max_blocks_per_seq,
@@ -720,6 +723,13 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         break;
     }
   }
+  return SIDP_OK;
+}
+
+int sidp_timing_select(sidp_handle* h, uint32_t class_mask) {
+  if (!h) return SIDP_EINVAL;
+  if (class_mask >> SIDP_NUM_KCLASSES) return SIDP_EINVAL;
+  h->timing_mask = class_mask;
   return SIDP_OK;
 }
 

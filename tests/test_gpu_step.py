@@ -260,6 +260,24 @@ def test_full_size_layer_sampled_rows(lib, name):
         st.close()
 
 
+def test_full_size_layer_batch512_sampled_rows(lib):
+    """The 70B layer at the largest benchmarked batch (512): four row blocks
+    per projection column tile and 512 sequences in the attention work list,
+    streamed through the ring; a few rows recomputed by the oracle."""
+    cfg = synth.get_config("llama70b_layer", batch=512)
+    st = Stack(cfg, keep_weights=False)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        rows = [0, 257, 511]
+        got = st.hidden.double().cpu().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        e = row_rel_err(got, want)
+        assert e.max() <= TIGHT, e
+    finally:
+        st.close()
+
+
 @pytest.mark.slow
 def test_qwen25_stack8_streamed_sampled_rows(lib):
     cfg = synth.get_config("qwen25_72b_stack8")
