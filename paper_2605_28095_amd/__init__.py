@@ -121,10 +121,14 @@ for _name, (_res, _args) in _sigs.items():
 
 
 def _ptr(x):
+    """Device (or host) address of a tensor for the C ABI, which takes dense
+    row-major buffers: a strided view would be read as if it were dense."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if not x.is_contiguous():
+        raise ValueError("the C ABI takes contiguous buffers; pass .contiguous()")
     return x.data_ptr()
 
 

@@ -177,14 +177,15 @@ struct sidp_handle {
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
   int fill_pct = 0;       // percent of the staged range in fill part A
-  // loads in flight per lane of the background fill: part A overlaps attention and may press harder;
-  // part B runs beside the projections, which lose more than the fill gains when it presses harder
+  // 16-byte loads in flight per lane of the background fill. Part A starts when
+  // the slot is released and mostly overlaps the next layer's QKV projection and
+  // KV append (latency-bound, spare bandwidth), so it may press harder; part B
+  // runs beside the projections, which lose more than the fill gains when it does.
   int fill_loads_a = 4, fill_loads_b = 2;
   // pooling: which part of a layer is staged, and which layers this rank owns
   int pool_mode = SIDP_POOL_LAYER;
   int ranks = 0, rank = 0;          // layer l is owned (never staged) when ranks > 0 and l % ranks == rank
   std::vector<int> streamed_layers;  // the layers that are staged, in order
-  bool events_ok = false;
   // ring state
   bool ring_started = false;
   int64_t ring_g = 0;  // global index of the next streamed layer
