@@ -274,6 +274,36 @@ def test_attention_block_permutation_invariance_bitexact(lib):
     assert np.array_equal(out1, out2)
 
 
+def test_attention_bad_block_index_is_reported(lib):
+    """A block index past the cache inside a sequence's attended range: the
+    kernel reads block 0 instead (never out of bounds) and latches the error,
+    which sync reports; a good call afterwards is clean."""
+    cfg = synth.get_config("llama70b_layer")
+    dev = _dev()
+    seqs = [40, 700]
+    ctx, tables, nblk, k, v, q, maxb = _attn_setup(lib, cfg, seqs)
+    B, Hq, Hkv, D = len(seqs), cfg["num_q_heads"], cfg["num_kv_heads"], cfg["head_dim"]
+    h = lib.sidp_create(lib.make_config(dict(cfg, num_layers=1), B, maxb * 16 + 16))
+    try:
+        kc = torch.zeros(1, nblk, Hkv, 16, D, dtype=torch.bfloat16, device=dev)
+        vc = torch.zeros(1, nblk, Hkv, D, 16, dtype=torch.bfloat16, device=dev)
+        kc[0] = k.to(dev)
+        vc[0] = v.to(dev).transpose(-1, -2)
+        lib.sidp_kv_attach(h, kc, vc, nblk, 1)
+        out = torch.empty(B, Hq, D, dtype=torch.bfloat16, device=dev)
+        pos = torch.tensor(ctx, dtype=torch.int32, device=dev)
+        bad = [list(r) for r in tables]
+        bad[1][3] = nblk + 5
+        lib.sidp_attention(h, q.to(dev), 0, pos, torch.tensor(bad, dtype=torch.int32, device=dev), maxb, B, out)
+        with pytest.raises(lib.SidpError) as e:
+            lib.sidp_sync(h)
+        assert e.value.code == lib.SIDP_EINVAL
+        lib.sidp_attention(h, q.to(dev), 0, pos, torch.tensor(tables, dtype=torch.int32, device=dev), maxb, B, out)
+        lib.sidp_sync(h)
+    finally:
+        lib.sidp_destroy(h)
+
+
 # ------------------------------------------------------------------ slot mapping, copy
 
 def test_slot_mapping_bitexact_and_error(lib, tiny_handle):
