@@ -233,6 +233,27 @@ def test_ffn_matches_transformers_mlp():
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
+def test_ffn_bf16_rounding_point():
+    """In bf16 mode the SwiGLU output is rounded before the down projection: the
+    result differs from the exact one, by at most the round-to-nearest bound
+    (half a bf16 ulp, 2^-9 relative, on every term), and the decode layer's FFN
+    (attention projections zeroed) is exactly this FFN of its normed input."""
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    wg, wu, wd = (od.bf16_bits_to_f64(lw[k]) for k in ("w_gate", "w_up", "w_down"))
+    h = od.round_to_bf16(od.rms_norm(x, od.bf16_bits_to_f64(lw["g_mlp"]), cfg["rms_eps"]))
+    yr = oracle.ffn(h, wg, wu, wd, round_bf16=True)
+    ye = oracle.ffn(h, wg, wu, wd, round_bf16=False)
+    a = od.swiglu(h, wg, wu)
+    bound = 2.0 ** -9 * (np.abs(a) @ np.abs(wd).T)
+    assert np.any(yr != ye)
+    assert np.all(np.abs(yr - ye) <= bound * (1 + 1e-12))
+    lz = dict(lw)
+    lz["w_o"] = np.zeros_like(lw["w_o"])
+    x2 = od.decode_layer(x, lz, cfg, kc.copy(), vc.copy(), ctx, tabs, round_bf16=True)
+    np.testing.assert_allclose(x2 - x, yr, rtol=1e-12, atol=1e-12)
+
+
 def test_cas_ffn_is_per_replica_ffn():
     """CaS fuses the replicas' rows into one FFN call and cuts the output back:
     every live replica gets exactly its own rows' FFN, in order, and dummy
