@@ -252,8 +252,9 @@ __device__ __forceinline__ int seq_parts(const AttnCall& a, int b) {
   return (seq + kPartTokens - 1) / kPartTokens;
 }
 
-// Items of sequence b are prefix[b] * Hkv .. prefix[b+1] * Hkv - 1, ordered
-// (partition, KV head); prefix[] is built in LDS once per workgroup.
+// Item i of the work list is (entry i / Hkv of the plan, KV head i % Hkv).
+// Two 4-wave workgroups per CU (the register cap keeps a wave at 248 VGPRs so
+// that a fill wave still fits beside two of them on a SIMD).
 template <int D>
 __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) k_attn(AttnCall a) {
   constexpr int KK = D / 32, JD = D / 16;

@@ -20,9 +20,12 @@
 //  * Loads go through raw buffer resources: addresses stay in scalar
 //    registers, and an offset past the buffer reads zeros (row and K tails).
 //  * When the column tiles alone cannot fill the 256 CUs (N = 8192 gives 32
-//    tiles), K is split; each split writes fp32 partials and a reduction
-//    kernel sums them in split order (deterministic, so streamed and resident
-//    runs are bit-identical) and applies the epilogue.
+//    tiles), K is split; each split writes fp32 partials, which are summed in
+//    split order (deterministic, so streamed and resident runs are
+//    bit-identical) with the epilogue applied, either by k_splitk_reduce here
+//    or by the kernel that consumes the result (the RoPE/KV-append kernel for
+//    QKV, the residual + RMSNorm reduction for O and down; LinearCall's
+//    defer_reduce and norm_out select this).
 #include <cstdlib>
 
 #include "common.h"
