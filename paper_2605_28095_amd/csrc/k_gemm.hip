@@ -326,8 +326,17 @@ int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int mblocks = (M + 127) / 128;
   const int KT = round_up(K, 64) / kBK;
   const int base = tiles * mblocks;
-  // 4-wave workgroups of up to 128 rows; two fit per CU.
-  const int target = 2 * num_cus;
+  // Enough splits for about one 4-wave workgroup per CU (two fit): each
+  // split writes fp32 partials for all M x N outputs, and at decode batches
+  // that traffic (O at B=256: 8 splits would write and re-read 67 MB beside
+  // 134 MB of weights) costs more than the second workgroup's latency hiding
+  // gains. SIDP_SPLIT_TARGET overrides the target, in percent of the CU count.
+  static int pct = -1;
+  if (pct < 0) {
+    const char* e = std::getenv("SIDP_SPLIT_TARGET");
+    pct = e ? std::max(10, std::atoi(e)) : 100;
+  }
+  const int target = pct * num_cus / 100;
   int s = (target + base / 2) / base;
   if (s < 1) s = 1;
   if (s > 16) s = 16;
