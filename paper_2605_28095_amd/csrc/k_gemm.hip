@@ -288,16 +288,35 @@ __global__ void k_splitk_reduce(GemmArgs a) {
   if (EPI == SIDP_EPI_SWIGLU) {
     const int pc = (c / 32) * 64 + (c % 32);
     float g = 0.f, u = 0.f;
-    for (int s = 0; s < a.splits; s++) {
-      const float* p = a.ws + ((int64_t)s * a.M + row) * NP + pc;
-      g += p[0];
-      u += p[32];
+    for (int s0 = 0; s0 < a.splits; s0 += 4) {  // four partials in flight, summed in split order
+      float pg[4], pu[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        if (s0 + j < a.splits) {
+          const float* p = a.ws + ((int64_t)(s0 + j) * a.M + row) * NP + pc;
+          pg[j] = p[0];
+          pu[j] = p[32];
+        }
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        if (s0 + j < a.splits) {
+          g += pg[j];
+          u += pu[j];
+        }
     }
     ((uint16_t*)a.out)[idx] = f2bf(silu_f(g) * u);
   } else {
     const int pc = (c / 64) * 64 + (c % 64);  // packed column of output n (identity)
     float v = 0.f;
-    for (int s = 0; s < a.splits; s++) v += a.ws[((int64_t)s * a.M + row) * NP + pc];
+    for (int s0 = 0; s0 < a.splits; s0 += 4) {  // four partials in flight, summed in split order
+      float pv[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        if (s0 + j < a.splits) pv[j] = a.ws[((int64_t)(s0 + j) * a.M + row) * NP + pc];
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        if (s0 + j < a.splits) v += pv[j];
+    }
     if (EPI == SIDP_EPI_BF16) {
       if (a.bias) v += bf2f(a.bias[c]);
       ((uint16_t*)a.out)[idx] = f2bf(v);

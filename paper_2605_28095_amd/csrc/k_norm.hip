@@ -63,13 +63,22 @@ __global__ void __launch_bounds__(kRrnThreads) k_reduce_resid_norm(const float* 
   for (int c = 0; c < kRrnMaxChunks; c++) {
     const int i = (threadIdx.x + c * kRrnThreads) * 4;
     if (i < n) {
+      // partials four splits at a time: the loads of a group are in flight
+      // together, the sum still runs in split order
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int sp = 0; sp < splits; sp++) {
-        const float4 p = *(const float4*)(ws + ((int64_t)sp * M + row) * NP + i);
-        acc.x += p.x;
-        acc.y += p.y;
-        acc.z += p.z;
-        acc.w += p.w;
+      for (int sp0 = 0; sp0 < splits; sp0 += 4) {
+        float4 p[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if (sp0 + j < splits) p[j] = *(const float4*)(ws + ((int64_t)(sp0 + j) * M + row) * NP + i);
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if (sp0 + j < splits) {
+            acc.x += p[j].x;
+            acc.y += p[j].y;
+            acc.z += p[j].z;
+            acc.w += p[j].w;
+          }
       }
       const float4 r = *(const float4*)(xr + i);
       v[c] = make_float4(r.x + acc.x, r.y + acc.y, r.z + acc.z, r.w + acc.w);

@@ -37,11 +37,23 @@ __global__ void __launch_bounds__(256) k_rope_append(RopeCall c) {
   uint16_t v0 = 0, v1 = 0;  // the bf16 projection output of this lane's pair
   if (act) {
     if (c.ws) {
+      // four splits' partials in flight at a time, summed in split order
       float s0 = 0.f, s1 = 0.f;
-      for (int sp = 0; sp < c.splits; sp++) {
-        const float* pr = c.ws + ((int64_t)sp * c.batch + b) * c.ws_np;
-        s0 += pr[col0];
-        s1 += pr[col1];
+      for (int sp0 = 0; sp0 < c.splits; sp0 += 4) {
+        float p0[4], p1[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if (sp0 + j < c.splits) {
+            const float* pr = c.ws + ((int64_t)(sp0 + j) * c.batch + b) * c.ws_np;
+            p0[j] = pr[col0];
+            p1[j] = pr[col1];
+          }
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if (sp0 + j < c.splits) {
+            s0 += p0[j];
+            s1 += p1[j];
+          }
       }
       if (c.bias) {
         s0 += bf2f(c.bias[col0]);
