@@ -231,6 +231,9 @@ def main():
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resident-compare", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only copy BYTES once through the library's copy kernel and exit: the known-size "
+                         "transfer that scales the HBM traffic counters")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -247,6 +250,16 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration > 0:
+        n = args.copy_calibration
+        src = torch.full((n,), 1, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        sidp.sidp_copy(src, dst, n, 1024)
+        torch.cuda.synchronize()
+        ok = bool(torch.equal(src, dst))
+        log(f"copy calibration: {n} bytes, 1024 workgroups, {'ok' if ok else 'MISMATCH'}")
+        sys.exit(0 if ok else 1)
     cfg = synth.get_config(args.workload)
     B, L = args.batch, cfg["num_layers"]
     ctx = synth.context_lengths(cfg, args.seed, B)
