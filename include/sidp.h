@@ -256,17 +256,13 @@ int sidp_cas_ffn(sidp_handle *h, int32_t layer, int32_t n_replicas, const void *
  * g + 1 is copied into the other slot as two tiles (§4.2 "tensor tiles", each
  * with its notification): tile A once layer g - 1 has released the slot, tile
  * B once layer g's attention half has been issued, so that it runs beside
- * layer g's projections. Compute waits for each tile just before the half
- * that reads it: tile A (which holds every weight of the attention half)
- * before the attention half, tile B before the projection half. Each op is
- * 3 int32 {kind, g, slot}; kinds:
- *   0 copy tile A of layer g, then mark it   1 copy tile B of layer g, then mark it
- *   2 compute waits for tile A               3 attention half of layer g
- *   4 mark attention half issued             5 projection half of layer g
- *   6 mark slot released                     7 copy stream waits for the release
+ * layer g's projections. Each op is 3 int32 {kind, g, slot}; kinds:
+ *   0 copy tile A of layer g          1 copy tile B of layer g, then mark filled
+ *   2 compute waits for the fill      3 attention half of layer g
+ *   4 mark attention half issued      5 projection half of layer g
+ *   6 mark slot released              7 copy stream waits for the release
  *   8 copy stream waits for the attention half
- *   9 an owned layer computed from the pool; g = call * num_layers + layer, slot -1
- *  10 compute waits for tile B.
+ *   9 an owned layer computed from the pool; g = call * num_layers + layer, slot -1.
  * ops (host, 3 * *n_ops int32) receives up to *n_ops ops; on return *n_ops is
  * the number written. SIDP_EINVAL if the capacity is too small or the
  * arguments are bad. */

@@ -14,12 +14,10 @@ Reading for one GPU with 2 slots: layers are numbered globally across decode
 iterations, g = step * L + l, and layer g uses slot g mod 2. While layer g
 computes, layer g + 1 is read into the other slot as two tiles: tile A as soon
 as layer g - 1 has released that slot, tile B once layer g's attention half
-has been issued (so that it overlaps layer g's projections). Each tile has its
-own notification, and compute waits for each just before it uses the tile:
-tile A (which holds every weight the attention half reads) before layer
-g + 1's attention half, tile B before its projection half. Before the first
-layer, layer 0 is read whole. The copy stream therefore always runs one layer
-ahead, also across the end of an iteration.
+has been issued (so that it overlaps layer g's projections). Layer g + 1's
+compute waits for tile B's notification. Before the first layer, layer 0 is
+read whole. The copy stream therefore always runs one layer ahead, also across
+the end of an iteration.
 
 Layers owned by this rank (§4.1: each rank keeps the FFN weights of the
 layers it owns, layer l being owned by rank l mod d when d ranks pool their
@@ -30,16 +28,15 @@ per step), and an owned layer's compute sits between the ring operations of
 its neighbours in layer order.
 
 Operations, in host issue order, as (kind, g, slot):
-  ("fill_a", g, s)     copy tile A of layer g mod L into slot s, then notify
-  ("fill_b", g, s)     copy tile B, then notify
-  ("wait_fill", g, s)  compute waits for layer g's tile A
+  ("fill_a", g, s)     copy tile A of layer g mod L into slot s
+  ("fill_b", g, s)     copy tile B, then notify "filled"
+  ("wait_fill", g, s)  compute waits for layer g's "filled"
   ("attn", g, s)       attention half of layer g
   ("mid", g, s)        compute notifies that the attention half is issued
   ("proj", g, s)       projection half of layer g
   ("done", g, s)       compute notifies that slot s is free
   ("wait_done", g, s)  copy waits for layer g's "done"
   ("wait_mid", g, s)   copy waits for layer g's "mid"
-  ("wait_fill_b", g, s)  compute waits for layer g's tile B
   ("local", n, -1)     compute of owned layer n (n = step * L + l), from the pool
 """
 
@@ -67,8 +64,7 @@ def was_schedule(num_layers, steps, ranks=0, rank=0):
             if g > 0:
                 ops.append(("wait_done", g - 1, n))
             ops += [("fill_a", g + 1, n), ("wait_fill", g, s), ("attn", g, s), ("mid", g, s),
-                    ("wait_mid", g, s), ("fill_b", g + 1, n), ("wait_fill_b", g, s), ("proj", g, s),
-                    ("done", g, s)]
+                    ("wait_mid", g, s), ("fill_b", g + 1, n), ("proj", g, s), ("done", g, s)]
             g += 1
     return ops
 

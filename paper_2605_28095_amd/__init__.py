@@ -38,7 +38,7 @@ SIDP_EPI_RESID = 1
 SIDP_EPI_SWIGLU = 2
 
 PLAN_OPS = {0: "fill_a", 1: "fill_b", 2: "wait_fill", 3: "attn", 4: "mid", 5: "proj", 6: "done", 7: "wait_done",
-            8: "wait_mid", 9: "local", 10: "wait_fill_b"}
+            8: "wait_mid", 9: "local"}
 
 SIDP_POOL_LAYER = 0
 SIDP_POOL_FFN = 1
@@ -219,7 +219,7 @@ def sidp_sync(h):
 
 def sidp_plan(num_layers, steps, ranks=0, rank=0):
     """Ring operations in issue order, as (kind name, g, slot)."""
-    cap = 10 * num_layers * steps + 2  # at most 10 ring ops per layer, plus the first fill
+    cap = 9 * num_layers * steps + 2
     buf = (ctypes.c_int32 * (3 * cap))()
     n = ctypes.c_int32(cap)
     _check(_lib.sidp_plan(num_layers, steps, ranks, rank, buf, ctypes.byref(n)), "sidp_plan")

@@ -82,14 +82,10 @@ bool config_ok(const sidp_config* c) {
 // into the other slot, in two parts: part A as soon as layer g - 1 has
 // released that slot, part B once layer g's attention half has been issued,
 // so that it runs beside the projections (MFMA-bound, spare HBM bandwidth).
-// Each part has its own event, and compute waits for each just before the
-// half that reads it: part A (every weight of the attention half) before the
-// attention half, part B before the projection half. Part B of layer g + 1
-// may therefore run on into layer g + 1's attention half.
 enum {
-  OP_FILL_A = 0,     // copy stream: first part of layer g's blob into slot, then mark it
-  OP_FILL_B = 1,     // copy stream: the rest, then mark it
-  OP_WAIT_FILL = 2,  // compute stream waits for part A of the slot's fill
+  OP_FILL_A = 0,     // copy stream: first part of layer g's blob into slot
+  OP_FILL_B = 1,     // copy stream: the rest, then mark the slot filled
+  OP_WAIT_FILL = 2,  // compute stream waits for the slot's fill
   OP_ATTN = 3,       // compute: attention half of layer g
   OP_MID = 4,        // compute: mark layer g's attention half issued
   OP_PROJ = 5,       // compute: projection half of layer g
@@ -97,7 +93,6 @@ enum {
   OP_WAIT_DONE = 7,  // copy stream waits for layer g to release its slot
   OP_WAIT_MID = 8,   // copy stream waits for layer g's attention half
   OP_LOCAL = 9,      // compute: a layer this rank owns, straight from the pool (g = step * L + layer)
-  OP_WAIT_FILL_B = 10,  // compute stream waits for part B of the slot's fill
 };
 struct RingOp {
   int kind;
@@ -119,7 +114,6 @@ void ring_layer(int64_t g, bool first, std::vector<RingOp>& ops) {
   ops.push_back({OP_MID, g, s});
   ops.push_back({OP_WAIT_MID, g, s});
   ops.push_back({OP_FILL_B, g + 1, n});
-  ops.push_back({OP_WAIT_FILL_B, g, s});
   ops.push_back({OP_PROJ, g, s});
   ops.push_back({OP_DONE, g, s});
 }
@@ -181,7 +175,7 @@ struct sidp_handle {
   float* cas_y = nullptr;  // owner-side FFN output of the concatenated CaS rows [max_batch][H] fp32
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
-  hipEvent_t filled_a[kSlots] = {}, filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
+  hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
   int fill_pct = 0;       // percent of the staged range in fill part A
   // 16-byte loads in flight per lane of the background fill. Part A starts when
   // the slot is released and mostly overlaps the next layer's QKV projection and
@@ -245,7 +239,6 @@ static void free_device(sidp_handle* h) {
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; i++) {
-    if (h->filled_a[i]) (void)hipEventDestroy(h->filled_a[i]);
     if (h->filled[i]) (void)hipEventDestroy(h->filled[i]);
     if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
     if (h->mid[i]) (void)hipEventDestroy(h->mid[i]);
@@ -323,7 +316,6 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   if (hipMemcpy(h->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess) return fail(SIDP_EHIP);
   if (hipMemcpy(h->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) return fail(SIDP_EHIP);
   for (int i = 0; i < kSlots; i++) {
-    if (hipEventCreateWithFlags(&h->filled_a[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->filled[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->mid[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
@@ -519,9 +511,7 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   const int H = c.hidden, D = c.head_dim;
   // a2: RMSNorm before attention; for layers after the first of a step the
   // previous layer's down-projection reduction has already written it
-  if (layer == 0)
-    TIMED(h, SIDP_K_NORM_ATTN, s,
-          launch_rmsnorm(hidden, h->g_attn_all + (size_t)layer * H, c.rms_eps, h->h, B, H, s));
+  if (layer == 0) TIMED(h, SIDP_K_NORM_ATTN, s, launch_rmsnorm(hidden, wb + L.g_attn, c.rms_eps, h->h, B, H, s));
   // a3: QKV projection (+ bias). With split-K its partials are reduced by the
   // RoPE kernel below, which rounds to bf16 exactly where the projection would.
   const uint16_t* qkv_bias = c.qkv_bias ? (const uint16_t*)(wb + L.bias) : nullptr;
@@ -615,15 +605,11 @@ static hipError_t run_layer(sidp_handle* h, const uint8_t* wb, int layer, float*
   return run_proj_half(h, wb, wb, layer, hidden, B, s);
 }
 
-// The staged byte range [lo, hi) of a layer blob and the end `mid` of fill
-// part A. When whole layers are staged, part A holds at least everything the
-// attention half reads from the slot (QK-norm gains, bias, W_qkv), since
-// compute waits only for part A before that half.
+// The staged byte range [lo, hi) of a layer blob and the end `mid` of fill part A.
 static void staged_range(const sidp_handle* h, size_t* lo, size_t* mid, size_t* hi) {
   *lo = h->pool_mode == SIDP_POOL_FFN ? h->blob.ffn_lo : 0;
   *hi = h->blob.total;
   *mid = std::min(*hi, *lo + align_up((*hi - *lo) * (size_t)h->fill_pct / 100, kAlign));
-  if (h->pool_mode != SIDP_POOL_FFN) *mid = std::max(*mid, h->blob.w_o);
 }
 
 // The layer that ring instance g computes.
@@ -641,7 +627,7 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   hipError_t e;
   if (part_a && (flags & SIDP_DEBUG_POISON))  // the whole slot, unstaged parts included
     if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
-  if (flags & SIDP_DEBUG_DELAY)  // before each part: a missing wait on either shows up as stale weights
+  if (part_a && (flags & SIDP_DEBUG_DELAY))
     if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
   if (hi <= lo) return hipSuccess;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
@@ -703,7 +689,6 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
     switch (op.kind) {
       case OP_FILL_A:
         HIPCHK(h, issue_fill(h, op.g, op.slot, st_lo, st_mid, flags, cp));
-        HIPCHK(h, hipEventRecord(h->filled_a[op.slot], cp));
         break;
       case OP_FILL_B:
         HIPCHK(h, issue_fill(h, op.g, op.slot, st_mid, st_hi, flags, cp));
@@ -711,11 +696,6 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         break;
       case OP_WAIT_FILL:
         // under SIDP_TIMING the interval around the wait is the compute stall on the fill
-        HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
-        HIPCHK(h, hipStreamWaitEvent(cs, h->filled_a[op.slot], 0));
-        HIPCHK(h, time_end(h, SIDP_K_WAIT_FILL, cs));
-        break;
-      case OP_WAIT_FILL_B:
         HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
         HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
         HIPCHK(h, time_end(h, SIDP_K_WAIT_FILL, cs));

@@ -275,10 +275,9 @@ def test_cas_ffn_is_per_replica_ffn():
 
 def test_was_schedule_ordering():
     """Properties the paper's buffer management requires, checked on the
-    issue order: compute waits for each tile of a layer before the half that
-    reads it (tile A before the attention half, tile B before the
-    projections), a slot is refilled only after its previous layer released
-    it, at most two layers occupy the cache, and the lookahead is one layer."""
+    issue order: every layer is fully read into its slot before compute on it
+    starts, a slot is refilled only after its previous layer released it, at
+    most two layers occupy the cache, and the lookahead is one layer."""
     L, steps = 5, 3
     ops = was_schedule(L, steps)
     total = L * steps
@@ -287,12 +286,10 @@ def test_was_schedule_ordering():
     for g in range(total):
         s = g % 2
         # compute on layer g: wait for its fill, then both halves, then release
-        seq = [pos[(k, g, s)] for k in ("wait_fill", "attn", "mid", "wait_fill_b", "proj", "done")]
+        seq = [pos[(k, g, s)] for k in ("wait_fill", "attn", "mid", "proj", "done")]
         assert seq == sorted(seq)
-        # each tile of layer g was issued before the wait on it, tile A first
-        assert pos[("fill_a", g, s)] < pos[("fill_b", g, s)]
-        assert pos[("fill_a", g, s)] < pos[("wait_fill", g, s)]
-        assert pos[("fill_b", g, s)] < pos[("wait_fill_b", g, s)]
+        # both tiles of layer g were issued before the wait on them
+        assert pos[("fill_a", g, s)] < pos[("fill_b", g, s)] < pos[("wait_fill", g, s)]
         if g >= 1:
             # tile A of layer g + 1 waits for layer g - 1 (same slot) to be released
             assert pos[("done", g - 1, (g + 1) % 2)] < pos[("wait_done", g - 1, (g + 1) % 2)]
