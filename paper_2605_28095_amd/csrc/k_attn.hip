@@ -170,10 +170,12 @@ __device__ __forceinline__ void load_chunk(const AttnCall& a, const ChunkSrc& sr
     const int64_t off = ((region_blk + blk[j]) * a.kv.hkv + src.g) * kBlockBytes;
     const char* kb = (const char*)a.kv.k + off;
     const char* vb = (const char*)a.kv.v + off;
+    // non-temporal: each KV byte is read once per layer, and streaming loads
+    // that do not allocate in the caches read HBM about 10% faster
 #pragma unroll
-    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = *(const u32x4_t*)(kb + k_lane + kk * 64);
+    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = __builtin_nontemporal_load((const u32x4_t*)(kb + k_lane + kk * 64));
 #pragma unroll
-    for (int jd = 0; jd < JD; jd++) c.v[jd][j] = *(const u32x2_t*)(vb + v_lane + jd * 512);
+    for (int jd = 0; jd < JD; jd++) c.v[jd][j] = __builtin_nontemporal_load((const u32x2_t*)(vb + v_lane + jd * 512));
   }
 }
 
