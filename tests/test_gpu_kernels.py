@@ -63,6 +63,8 @@ LINEAR_CASES = [
     (300, 512, 640, 1, False),     # two row blocks, ragged
     (512, 1024, 512, 2, False),
     (17, 4096, 2048, 1, False),
+    (128, 3072, 1024, 1, False),   # three k-tiles per split: whole rounds of the three-deep ring only
+    (100, 256, 45056, 0, True),    # enough column tiles for one split
 ]
 
 
