@@ -31,6 +31,7 @@ constexpr int kSlots = 2;
 constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
 constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
+constexpr int kFillSmallBatch = 128;   // below this many rows the fill runs with more loads in flight
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
@@ -181,7 +182,10 @@ struct sidp_handle {
   // the slot is released and mostly overlaps the next layer's QKV projection and
   // KV append (latency-bound, spare bandwidth), so it may press harder; part B
   // runs beside the projections, which lose more than the fill gains when it does.
-  int fill_loads_a = 4, fill_loads_b = 2;
+  // Below kFillSmallBatch rows a layer computes in less time than its fill takes,
+  // so both parts press harder there. 0: that per-batch default; else a fixed count.
+  int fill_loads_a = 0, fill_loads_b = 0;
+  int step_batch = 0;  // rows of the decode step being issued
   // pooling: which part of a layer is staged, and which layers this rank owns
   int pool_mode = SIDP_POOL_LAYER;
   int ranks = 0, rank = 0;          // layer l is owned (never staged) when ranks > 0 and l % ranks == rank
@@ -633,7 +637,12 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
-  else e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? h->fill_loads_a : h->fill_loads_b, cp);
+  else {
+    const bool small = h->step_batch < kFillSmallBatch;
+    const int la = h->fill_loads_a ? h->fill_loads_a : (small ? 8 : 4);
+    const int lb = h->fill_loads_b ? h->fill_loads_b : (small ? 4 : 2);
+    e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? la : lb, cp);
+  }
   if (e != hipSuccess) return e;
   return time_end(h, SIDP_K_FILL, cp);
 }
@@ -652,6 +661,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   if (parts > h->attn_max_parts) return SIDP_EINVAL;
   const bool streamed = flags & SIDP_STREAMED;
   h->timing = (flags & SIDP_TIMING) != 0;
+  h->step_batch = batch;
   hipStream_t cs = (hipStream_t)compute, cp = (hipStream_t)copy;
   if (streamed && (!h->slots || cp == cs)) return SIDP_EINVAL;
   h->last_compute = cs;
