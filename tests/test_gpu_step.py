@@ -87,11 +87,14 @@ def test_small_stack_multi_step_vs_oracle(lib, variant):
         st.close()
 
 
-def test_streamed_equals_resident_bitexact(lib):
+@pytest.mark.parametrize("batch", [8, 160])
+def test_streamed_equals_resident_bitexact(lib, batch):
     """Weights served from the 2-slot ring give the same bits as weights read
     in place, even with every slot poisoned (NaN) and each fill delayed before
-    it lands: a missing wait would surface as NaN or as stale weights."""
-    cfg = _small_stack_cfg(num_layers=5)
+    it lands: a missing wait would surface as NaN or as stale weights. Both
+    batches, on either side of 128 rows, where the fill changes its loads in
+    flight per lane."""
+    cfg = _small_stack_cfg(num_layers=5, batch=batch, num_phys_blocks=None if batch > 8 else 64)
     st = Stack(cfg, gains="random", regions=2, reserve=2)
     try:
         copy = torch.cuda.Stream()
