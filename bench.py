@@ -309,7 +309,7 @@ def main():
         for r in sample_rows:
             tabs_rows.append(list(range(o, o + need[r])) + [-1] * (width - need[r]))
             o += need[r]
-    dec.k_view()[0].copy_(k0)
+    dec.set_k_natural(0, k0)
     dec.v_view()[0].copy_(v0.transpose(-1, -2))
     del k0, v0
     for r in range(1, R):  # every region holds the same content; each layer still reads its own region

@@ -162,8 +162,11 @@ int sidp_kv_alloc(int32_t batch, const int32_t *ctx_lens, int32_t reserve_tokens
 size_t sidp_kv_region_bytes(const sidp_config *cfg, int32_t num_phys_blocks);
 /* Registers caller-owned KV caches of num_regions regions each. Layer l reads
  * and writes region l % num_regions. Layouts (bf16):
- *   K: [region][block][kv_head][token in block][d]
+ *   K: [region][block][kv_head][d / 8][token in block][d % 8]
  *   V: [region][block][kv_head][d][token in block]   (transposed per block)
+ * Both keep a (block, kv_head) pair's tokens in one contiguous
+ * block_size * D * 2-byte piece; the orders inside it are the ones the
+ * attention kernel's matrix fragments read as whole contiguous runs.
  * Cached keys are stored after RoPE (and after QK-norm when enabled). */
 int sidp_kv_attach(sidp_handle *h, void *k_cache, void *v_cache, int32_t num_phys_blocks, int32_t num_regions);
 

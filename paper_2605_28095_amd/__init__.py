@@ -303,4 +303,4 @@ def raw_call(name, *args):
     return getattr(_lib, name)(*args)
 
 
-from .model import WaSDecoder  # noqa: E402,F401
+from .model import WaSDecoder, k_blocks_from_lib, k_blocks_to_lib  # noqa: E402,F401

@@ -42,7 +42,7 @@ hipError_t launch_reduce_resid_norm(const float* ws, int splits, int M, int NP, 
                                     float eps, void* h, hipStream_t s);
 
 struct KvView {
-  uint16_t* k;            // [regions][nblk][Hkv][bs][D]
+  uint16_t* k;            // [regions][nblk][Hkv][D / 8][bs][8]
   uint16_t* v;            // [regions][nblk][Hkv][D][bs]
   int nblk, regions;
   int hkv, d, bs;

@@ -173,7 +173,7 @@ __device__ __forceinline__ void load_chunk(const AttnCall& a, const ChunkSrc& sr
     // non-temporal: each KV byte is read once per layer, and streaming loads
     // that do not allocate in the caches read HBM about 10% faster
 #pragma unroll
-    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = __builtin_nontemporal_load((const u32x4_t*)(kb + k_lane + kk * 64));
+    for (int kk = 0; kk < KK; kk++) c.k[j][kk] = __builtin_nontemporal_load((const u32x4_t*)(kb + k_lane + kk * 1024));
 #pragma unroll
     for (int jd = 0; jd < JD; jd++) c.v[jd][j] = __builtin_nontemporal_load((const u32x2_t*)(vb + v_lane + jd * 512));
   }
@@ -308,8 +308,11 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
   };
 
   // K fragment: token lane & 15, dims (lane >> 4) * 8 + 32 kk; V^T fragment:
-  // dim 16 jd + (lane & 15), tokens (lane >> 4) * 4 .. + 3 (byte offsets)
-  const uint32_t k_lane = (uint32_t)(head * D + lg * 8) * 2u;
+  // dim 16 jd + (lane & 15), tokens (lane >> 4) * 4 .. + 3 (byte offsets).
+  // K blocks are stored [d / 8][token][d % 8], so the K fragment of MFMA kk is
+  // the contiguous 1 KB run of 16-byte pieces 64 kk + lane: whole cache lines
+  // per load instruction, which streaming (non-temporal) loads need.
+  const uint32_t k_lane = (uint32_t)lane * 16u;
   const uint32_t v_lane = (uint32_t)(head * 16 + lg * 4) * 2u;
   bool bad = false;
   int round = 0;

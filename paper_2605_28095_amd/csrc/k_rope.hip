@@ -96,10 +96,12 @@ __global__ void __launch_bounds__(256) k_rope_append(RopeCall c) {
     qo[lane] = f2bf(y0);
     qo[lane + half] = f2bf(y1);
   } else if (ok_blk) {
+    // key blocks are [d / 8][token][d % 8]
     const int kh = h - c.hq;
-    uint16_t* kb = c.kv.k + (((region_base + blk) * c.kv.hkv + kh) * c.kv.bs + off) * (int64_t)D;
-    kb[lane] = f2bf(y0);
-    kb[lane + half] = f2bf(y1);
+    uint16_t* kb = c.kv.k + ((region_base + blk) * c.kv.hkv + kh) * (int64_t)D * c.kv.bs;
+    const int d0 = lane, d1 = lane + half;
+    kb[((d0 >> 3) * c.kv.bs + off) * 8 + (d0 & 7)] = f2bf(y0);
+    kb[((d1 >> 3) * c.kv.bs + off) * 8 + (d1 & 7)] = f2bf(y1);
   }
 }
 

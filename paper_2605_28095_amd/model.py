@@ -20,6 +20,20 @@ from . import (
 )
 
 
+def k_blocks_to_lib(k):
+    """Key blocks from the natural layout [..., block, kv_head, token, d] to the
+    library's [..., block, kv_head, d / 8, token, d % 8] (a view; copy_ it into
+    the cache)."""
+    *lead, bs, d = k.shape
+    return k.reshape(*lead, bs, d // 8, 8).transpose(-3, -2)
+
+
+def k_blocks_from_lib(kl):
+    """Key blocks from the library's layout back to [..., block, kv_head, token, d]."""
+    *lead, d8, bs, e = kl.shape
+    return kl.transpose(-3, -2).reshape(*lead, bs, d8 * e)
+
+
 class WaSDecoder:
     """A weight pool of num_layers packed layer blobs, a 2-slot weight cache,
     and num_regions paged KV regions of num_phys_blocks blocks each.
@@ -52,9 +66,18 @@ class WaSDecoder:
 
     # Cache views in the library's layouts.
     def k_view(self):
+        """K blocks are stored [region][block][kv_head][d / 8][token][d % 8]."""
         c = self.cfg
-        return self.k_cache.view(self.num_regions, self.num_phys_blocks, c["num_kv_heads"], c["block_size"],
-                                 c["head_dim"])
+        return self.k_cache.view(self.num_regions, self.num_phys_blocks, c["num_kv_heads"], c["head_dim"] // 8,
+                                 c["block_size"], 8)
+
+    def k_natural(self, region):
+        """Region `region` of the K cache as [block][kv_head][token][d] (a copy)."""
+        return k_blocks_from_lib(self.k_view()[region])
+
+    def set_k_natural(self, region, k):
+        """Writes key blocks given as [block][kv_head][token][d] into region `region`."""
+        self.k_view()[region].copy_(k_blocks_to_lib(k))
 
     def v_view(self):
         """V blocks are stored transposed: [region][block][kv_head][d][token]."""

@@ -72,8 +72,9 @@ class Stack:
     """A decoder stack set up on the GPU from seeded inputs.
 
     The KV content of every region is drawn by synth.kv_prefill in the
-    token-major block layout and written into the library's caches (V blocks
-    transposed, as the library stores them). `kv_natural[r]` keeps the
+    token-major block layout and written into the library's caches in the
+    layouts it stores them in (K as [d / 8][token][d % 8] per block, V
+    transposed). `kv_natural[r]` keeps the
     generator's tensors for the oracle.
     """
 
@@ -107,7 +108,7 @@ class Stack:
         self.kv_natural = []
         for r in range(regions):
             k, v = synth.kv_prefill(cfg, self.nblk, r, seed, device=self.gen_device)
-            self.dec.k_view()[r].copy_(k.to(self.device))
+            self.dec.set_k_natural(r, k.to(self.device))
             self.dec.v_view()[r].copy_(v.to(self.device).transpose(-1, -2))
             self.kv_natural.append((k, v))
         self.x0 = synth.hidden_input(cfg, seed, device=self.gen_device, batch=self.batch)
@@ -129,7 +130,7 @@ class Stack:
         """Restore hidden states and KV caches to the generated inputs."""
         self.hidden.copy_(self.x0.to(self.device))
         for r, (k, v) in enumerate(self.kv_natural):
-            self.dec.k_view()[r].copy_(k.to(self.device))
+            self.dec.set_k_natural(r, k.to(self.device))
             self.dec.v_view()[r].copy_(v.to(self.device).transpose(-1, -2))
         torch.cuda.synchronize()
 

@@ -140,7 +140,7 @@ def test_rope_append_parity(lib, name, qk_norm):
     cfgm = dict(cfg, num_layers=1)
     h = lib.sidp_create(lib.make_config(cfgm, B, 2048))
     try:
-        kc = torch.full((R, nblk, Hkv, 16, D), float("nan"), dtype=torch.bfloat16, device=dev)
+        kc = torch.full((R, nblk, Hkv, D // 8, 16, 8), float("nan"), dtype=torch.bfloat16, device=dev)
         vc = torch.full((R, nblk, Hkv, D, 16), float("nan"), dtype=torch.bfloat16, device=dev)
         lib.sidp_kv_attach(h, kc, vc, nblk, R)
         g = torch.Generator().manual_seed(11)
@@ -150,7 +150,7 @@ def test_rope_append_parity(lib, name, qk_norm):
         q_out = torch.empty(B, Hq, D, dtype=torch.bfloat16, device=dev)
         bt = torch.tensor(tables, dtype=torch.int32, device=dev)
         pos = torch.tensor(ctx, dtype=torch.int32, device=dev)
-        kc0, vc0 = bits(kc), bits(vc)
+        kc0, vc0 = bits(lib.k_blocks_from_lib(kc)), bits(vc)
         lib.sidp_rope_append(h, qkv.to(dev), pos, bt, 64, B, gq.to(dev), gk.to(dev), region, q_out)
         lib.sidp_sync(h)
         qf = f64(qkv)
@@ -163,7 +163,7 @@ def test_rope_append_parity(lib, name, qk_norm):
         q = oracle.rope_rotate_half(q, ctx[:, None], cfg["rope_theta"])
         k = oracle.rope_rotate_half(k, ctx[:, None], cfg["rope_theta"])
         assert_bf16_within_ulp(bits(q_out), q, what="rotated q")
-        kc1, vc1 = bits(kc), bits(vc)
+        kc1, vc1 = bits(lib.k_blocks_from_lib(kc)), bits(vc)
         expect_k, expect_v = kc0.copy(), vc0.copy()
         for b in range(B):
             p = int(ctx[b])
@@ -208,9 +208,9 @@ def _attn_run(lib, cfg, ctx, tables, nblk, k, v, q, maxb, regions=1, region=0):
     Hq, Hkv, D = cfg["num_q_heads"], cfg["num_kv_heads"], cfg["head_dim"]
     h = lib.sidp_create(lib.make_config(dict(cfg, num_layers=1), B, maxb * 16 + 16))
     try:
-        kc = torch.zeros(regions, nblk, Hkv, 16, D, dtype=torch.bfloat16, device=dev)
+        kc = torch.zeros(regions, nblk, Hkv, D // 8, 16, 8, dtype=torch.bfloat16, device=dev)
         vc = torch.zeros(regions, nblk, Hkv, D, 16, dtype=torch.bfloat16, device=dev)
-        kc[region] = k.to(dev)
+        kc[region] = lib.k_blocks_to_lib(k.to(dev))
         vc[region] = v.to(dev).transpose(-1, -2)
         lib.sidp_kv_attach(h, kc, vc, nblk, regions)
         out = torch.empty(B, Hq, D, dtype=torch.bfloat16, device=dev)
@@ -287,9 +287,9 @@ def test_attention_bad_block_index_is_reported(lib):
     B, Hq, Hkv, D = len(seqs), cfg["num_q_heads"], cfg["num_kv_heads"], cfg["head_dim"]
     h = lib.sidp_create(lib.make_config(dict(cfg, num_layers=1), B, maxb * 16 + 16))
     try:
-        kc = torch.zeros(1, nblk, Hkv, 16, D, dtype=torch.bfloat16, device=dev)
+        kc = torch.zeros(1, nblk, Hkv, D // 8, 16, 8, dtype=torch.bfloat16, device=dev)
         vc = torch.zeros(1, nblk, Hkv, D, 16, dtype=torch.bfloat16, device=dev)
-        kc[0] = k.to(dev)
+        kc[0] = lib.k_blocks_to_lib(k.to(dev))
         vc[0] = v.to(dev).transpose(-1, -2)
         lib.sidp_kv_attach(h, kc, vc, nblk, 1)
         out = torch.empty(B, Hq, D, dtype=torch.bfloat16, device=dev)

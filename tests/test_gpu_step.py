@@ -54,7 +54,7 @@ def test_tiny_layer_step_vs_oracle(lib, flags):
         want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
         _check_hidden(got, want, want_exact, "tiny layer")
         # the new token's key and value landed in the right slots
-        kc, vc = bits(st.dec.k_view()[0]), bits(st.dec.v_view()[0])
+        kc, vc = bits(st.dec.k_natural(0)), bits(st.dec.v_view()[0])
         for b in rows:
             p = int(st.ctx[b])
             blk, cblk = st.tables[b][p // 16], tabs[b][p // 16]
