@@ -108,3 +108,26 @@ def test_null_handle_calls_are_rejected():
     assert sidp.raw_call("sidp_destroy", None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_decode_step", None, None, None, None, 1, 1, 0, None, None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_plan", 0, 1, 0, 0, None, None) == sidp.SIDP_EINVAL
+
+
+def test_key_block_layout_helpers():
+    """Key blocks in the library's layout: element (token t, dim d) of a
+    (block, kv head) piece sits at ((d // 8) * block_size + t) * 8 + d % 8, so
+    the 16 tokens x 32 dims of one QK fragment are one contiguous 1 KB run."""
+    import torch
+    import paper_2605_28095_amd as sidp
+    nblk, hkv, bs, d = 3, 2, 16, 128
+    k = torch.arange(nblk * hkv * bs * d, dtype=torch.int64).reshape(nblk, hkv, bs, d)
+    kl = sidp.k_blocks_to_lib(k).contiguous()
+    assert kl.shape == (nblk, hkv, d // 8, bs, 8)
+    flat = kl.reshape(nblk, hkv, -1)
+    for t, dd in [(0, 0), (15, 127), (7, 45), (9, 8), (3, 100)]:
+        assert flat[2, 1, ((dd // 8) * bs + t) * 8 + dd % 8] == k[2, 1, t, dd]
+    # fragment kk of lane (token t, group g) covers dims 32 kk + 8 g .. + 7: 16-byte piece 64 kk + 16 g + t
+    pieces = flat[1, 0].reshape(-1, 8)
+    for kk in range(d // 32):
+        run = pieces[64 * kk:64 * kk + 64]
+        for lane in (0, 17, 63):
+            g, t = lane // 16, lane % 16
+            assert torch.equal(run[lane], k[1, 0, t, 32 * kk + 8 * g:32 * kk + 8 * g + 8])
+    assert torch.equal(sidp.k_blocks_from_lib(kl), k)
