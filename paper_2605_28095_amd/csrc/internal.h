@@ -33,6 +33,9 @@ size_t packed_bytes(int n, int k);
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus);
 size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus);
 hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s);
+// W_q [nq, k], W_k and W_v [nkv, k] packed as the one stacked matrix [nq + 2 nkv, k]
+hipError_t launch_pack_qkv(const void* wq, const void* wk, const void* wv, int nq, int nkv, int k, void* packed,
+                           hipStream_t s);
 hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, void* packed, hipStream_t s);
 hipError_t launch_linear(const LinearCall& c, hipStream_t s);
 

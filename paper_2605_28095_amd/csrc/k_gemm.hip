@@ -5,10 +5,11 @@
 // (8..512) and N, K in the thousands, so the weights dominate the bytes and
 // every weight byte must be read exactly once. Design:
 //  * Weights are packed once (into the layer's pool blob) in MFMA B-fragment
-//    order: for each group of 64 output columns, for each 16-wide k step,
-//    two 32x16 fragments of 64 lanes x 8 bf16. A wave that owns a column
-//    group streams its weights with 1 KB fully contiguous loads straight
-//    into registers; no LDS traffic for W.
+//    order: for each 64-wide k-tile, for each group of 64 output columns, for
+//    each 16-wide k step, two 32x16 fragments of 64 lanes x 8 bf16. A wave
+//    that owns a column group streams its weights with 1 KB fully contiguous
+//    loads straight into registers (no LDS traffic for W), and the waves of a
+//    grid, which move through k together, read adjacent 8 KB pieces.
 //  * Activations X are shared by the 4 waves of a workgroup: staged through
 //    LDS (64-wide k tiles, double buffered). A row is 128 bytes; its 16-byte
 //    chunk c is stored at slot c ^ ((row >> 1) & 7), so the 16 lanes that one
@@ -41,21 +42,42 @@ __host__ __device__ inline int round_up(int a, int b) { return (a + b - 1) / b *
 
 // ---------------------------------------------------------------- packing
 
-// W [N, K] -> packed [NP/64][KP/16][2][64][8], zero padded.
-__global__ void k_pack_linear(const uint16_t* __restrict__ w, int N, int K, int KB,
-                              int NG, uint16_t* __restrict__ out) {
+// Packed order of one 16-byte chunk: [KP/64 k-tiles][NG column groups][4 k
+// steps][2 column halves][64 lanes] of 8 bf16 each. A k-tile's 8 KB for every
+// column group are adjacent, so the waves of a grid that all stand at the same
+// k-tile read one contiguous stretch of the weights (spread over every HBM
+// channel) rather than one 8 KB piece in each of NG regions a group apart.
+__device__ __forceinline__ void packed_coords(int64_t chunk, int NG, int& lane, int& nf, int& kb, int& ng) {
+  lane = (int)(chunk % 64);
+  nf = (int)((chunk / 64) % 2);
+  const int ks = (int)((chunk / 128) % 4);
+  ng = (int)((chunk / 512) % NG);
+  kb = (int)(chunk / (512 * (int64_t)NG)) * 4 + ks;
+}
+
+// Rows of the matrix to pack, taken from up to three sources stacked in
+// order (the QKV projection packs W_q, W_k, W_v as one matrix).
+struct PackRows {
+  const uint16_t* w[3];
+  int n[3];  // rows from each source; the packed matrix has n[0] + n[1] + n[2]
+};
+
+// W [N, K] (the stacked sources) -> packed as above, zero padded.
+__global__ void k_pack_linear(PackRows src, int N, int K, int KB, int NG, uint16_t* __restrict__ out) {
   const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // one 8-element chunk
   const int64_t total = (int64_t)NG * KB * 2 * 64;
   if (chunk >= total) return;
-  const int lane = (int)(chunk % 64);
-  const int nf = (int)((chunk / 64) % 2);
-  const int kb = (int)((chunk / 128) % KB);
-  const int ng = (int)(chunk / (128 * (int64_t)KB));
-  const int n = ng * 64 + nf * 32 + (lane % 32);
+  int lane, nf, kb, ng;
+  packed_coords(chunk, NG, lane, nf, kb, ng);
+  int n = ng * 64 + nf * 32 + (lane % 32);
+  const bool in_rows = n < N;
+  int seg = 0;
+  while (seg < 2 && n >= src.n[seg]) n -= src.n[seg++];
+  const uint16_t* w = src.w[seg];
   const int k0 = kb * 16 + (lane / 32) * 8;
   uint16_t v[8];
 #pragma unroll
-  for (int i = 0; i < 8; i++) v[i] = (n < N && k0 + i < K) ? w[(int64_t)n * K + k0 + i] : (uint16_t)0;
+  for (int i = 0; i < 8; i++) v[i] = (in_rows && k0 + i < K) ? w[(int64_t)n * K + k0 + i] : (uint16_t)0;
   uint16_t* dst = out + chunk * 8;
 #pragma unroll
   for (int i = 0; i < 8; i++) dst[i] = v[i];
@@ -67,10 +89,8 @@ __global__ void k_pack_gate_up(const uint16_t* __restrict__ wg, const uint16_t* 
   const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t total = (int64_t)NG * KB * 2 * 64;
   if (chunk >= total) return;
-  const int lane = (int)(chunk % 64);
-  const int nf = (int)((chunk / 64) % 2);
-  const int kb = (int)((chunk / 128) % KB);
-  const int ng = (int)(chunk / (128 * (int64_t)KB));
+  int lane, nf, kb, ng;
+  packed_coords(chunk, NG, lane, nf, kb, ng);
   const int f = ng * 32 + (lane % 32);
   const int k0 = kb * 16 + (lane / 32) * 8;
   const uint16_t* src = nf == 0 ? wg : wu;
@@ -149,8 +169,9 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
 
   const __amdgpu_buffer_rsrc_t xr_rsrc = make_rsrc(a.x, (uint32_t)((size_t)a.M * a.K * 2));
   const __amdgpu_buffer_rsrc_t wr_rsrc = make_rsrc(a.w, (uint32_t)((size_t)a.NG * a.KP * 64 * 2));
-  // byte offset of this wave's weight stream: column group ng, 8 fragments (1 KB) per k-tile
-  const uint32_t w_base = (uint32_t)(active ? ng : 0) * (uint32_t)(a.KP / kBK) * 8192u;
+  // byte offset of this wave's 8 KB piece of k-tile kt: (kt * NG + ng) * 8 KB
+  const uint32_t w_base = (uint32_t)(active ? ng : 0) * 8192u;
+  const uint32_t w_tile = (uint32_t)a.NG * 8192u;
   const uint32_t w_lane = (uint32_t)lane * 16u;
 
   // X chunks this thread stages: row r, 16-byte column chunk cc of the 64-wide k tile
@@ -195,7 +216,7 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
   };
   // fragments (kb, nf) of tile kt live at 1 KB * (kb * 2 + nf) in the tile's 8 KB
   auto load_w_half = [&](int kt, int half, u32x4_t (&w)[4]) {
-    const uint32_t soff = w_base + (uint32_t)kt * 8192u + (uint32_t)half * 4096u;
+    const uint32_t soff = w_base + (uint32_t)kt * w_tile + (uint32_t)half * 4096u;
 #pragma unroll
     for (int j = 0; j < 4; j++) w[j] = buf_load16(wr_rsrc, w_lane + j * 1024u, soff);
   };
@@ -369,11 +390,22 @@ size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus) {
   return (size_t)s * M * round_up(n_cols_packed, 64) * sizeof(float);
 }
 
-hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s) {
+static hipError_t launch_pack_rows(const PackRows& src, int n, int k, void* packed, hipStream_t s) {
   const int NG = round_up(n, 64) / 64, KB = round_up(k, 64) / 16;
   const int64_t chunks = (int64_t)NG * KB * 128;
-  k_pack_linear<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>((const uint16_t*)w, n, k, KB, NG, (uint16_t*)packed);
+  k_pack_linear<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(src, n, k, KB, NG, (uint16_t*)packed);
   return hipGetLastError();
+}
+
+hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s) {
+  PackRows src{{(const uint16_t*)w, nullptr, nullptr}, {n, 0, 0}};
+  return launch_pack_rows(src, n, k, packed, s);
+}
+
+hipError_t launch_pack_qkv(const void* wq, const void* wk, const void* wv, int nq, int nkv, int k, void* packed,
+                           hipStream_t s) {
+  PackRows src{{(const uint16_t*)wq, (const uint16_t*)wk, (const uint16_t*)wv}, {nq, nkv, nkv}};
+  return launch_pack_rows(src, nq + 2 * nkv, k, packed, s);
 }
 
 hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, void* packed, hipStream_t s) {

@@ -384,9 +384,7 @@ int sidp_pool_load_layer(sidp_handle* h, int32_t layer, const sidp_layer_weights
   // Fused QKV: the q, k and v row blocks are multiples of 64 rows, so their
   // packed forms concatenate along the column groups.
   uint8_t* wqkv = base + h->blob.w_qkv;
-  HIPCHK(h, launch_pack_linear(w->w_q, (int)QD, (int)H, wqkv, s));
-  HIPCHK(h, launch_pack_linear(w->w_k, (int)KD, (int)H, wqkv + packed_bytes((int)QD, (int)H), s));
-  HIPCHK(h, launch_pack_linear(w->w_v, (int)KD, (int)H, wqkv + packed_bytes((int)(QD + KD), (int)H), s));
+  HIPCHK(h, launch_pack_qkv(w->w_q, w->w_k, w->w_v, (int)QD, (int)KD, (int)H, wqkv, s));
   HIPCHK(h, launch_pack_linear(w->w_o, (int)H, (int)QD, base + h->blob.w_o, s));
   HIPCHK(h, launch_pack_gate_up(w->w_gate, w->w_up, c.ffn_dim, (int)H, base + h->blob.w_gu, s));
   HIPCHK(h, launch_pack_linear(w->w_down, (int)H, c.ffn_dim, base + h->blob.w_d, s));
