@@ -15,9 +15,9 @@
 //    chunk c is stored at slot c ^ ((row >> 1) & 7), so the 16 lanes that one
 //    LDS cycle serves for a 128-bit fragment read (rows r..r+15, one chunk)
 //    hit 16 distinct 16-byte bank groups of the 64 four-byte banks.
-//  * A workgroup covers up to 256 rows x 256 columns with 4 or 8 waves; each
-//    wave holds MF x 2 accumulators of 32x32 (up to 128 rows x 64 columns)
-//    and issues v_mfma_f32_32x32x16_bf16; two waves share each SIMD.
+//  * A workgroup covers up to 128 rows x 256 columns with 4 waves; each wave
+//    holds MF x 2 accumulators of 32x32 (up to 128 rows x 64 columns) and
+//    issues v_mfma_f32_32x32x16_bf16; two workgroups fit on a CU.
 //  * Loads go through raw buffer resources: addresses stay in scalar
 //    registers, and an offset past the buffer reads zeros (row and K tails).
 //  * When the column tiles alone cannot fill the 256 CUs (N = 8192 gives 32
@@ -132,12 +132,12 @@ __device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-// One workgroup: WM x 4 waves. Wave (wm, wn) computes rows
-// [row0 + wm*MF*32, +MF*32) x the 64 packed columns of group tile*4 + wn.
-template <int MF, int WM, int EPI, bool PARTIAL>
-__global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm(GemmArgs a) {
-  constexpr int NT = 256 * WM;
-  constexpr int BM = WM * MF * 32;
+// One workgroup: 4 waves. Wave wn computes rows [row0, row0 + MF*32) x the
+// 64 packed columns of group tile*4 + wn.
+template <int MF, int EPI, bool PARTIAL>
+__global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs a) {
+  constexpr int NT = 256;
+  constexpr int BM = MF * 32;
   constexpr int CPT = BM * 8 / NT;  // 16-byte X chunks per thread per stage (= MF)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   uint16_t* lds0 = smem;
@@ -160,7 +160,7 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
   const int row0 = mblk * BM;
   // wave index made provably uniform so weight offsets live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wn = wave;
   const int ng = tile * kWaves + wn;
   const bool active = ng < a.NG;
   const int KT = a.KP / kBK;
@@ -191,7 +191,7 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
 #pragma unroll
       for (int r = 0; r < 16; r++) acc[m][n][r] = 0.f;
 
-  const int arow = wm * MF * 32 + (lane & 31);
+  const int arow = lane & 31;
   u32x4_t xs[CPT];
   // Weight fragments of a k-tile in two halves (k steps 0-1 and 2-3). The
   // next tile's low half is fetched at the top of an iteration, its high half
@@ -269,7 +269,7 @@ __global__ void __launch_bounds__(256 * WM, (WM == 1 && MF <= 4) ? 2 : 1) k_gemm
   for (int m = 0; m < MF; m++) {
 #pragma unroll
     for (int r = 0; r < 16; r++) {
-      const int row = row0 + wm * MF * 32 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      const int row = row0 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
       if (row >= a.M) continue;
       if (PARTIAL) {
         float* dst = a.ws + ((int64_t)split * a.M + row) * NP + ng * 64 + (lane & 31);
@@ -351,14 +351,6 @@ __global__ void k_splitk_reduce(GemmArgs a) {
 
 size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k, 64) * 2; }
 
-static int gemm_variant() {
-  static int v = -1;
-  if (v < 0) {
-    const char* e = std::getenv("SIDP_GEMM_VARIANT");
-    v = e ? std::atoi(e) : 0;
-  }
-  return v;
-}
 
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int NG = round_up(n_cols_packed, 64) / 64;
@@ -417,30 +409,29 @@ hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, voi
   return hipGetLastError();
 }
 
-template <int MF, int WM, int EPI, bool P>
+template <int MF, int EPI, bool P>
 static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
-  constexpr int BM = WM * MF * 32;
+  constexpr int BM = MF * 32;
   a.mblocks = (a.M + BM - 1) / BM;
-  const size_t lds = (size_t)2 * WM * MF * 32 * kBK * sizeof(uint16_t);
+  const size_t lds = (size_t)2 * BM * kBK * sizeof(uint16_t);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e =
-        hipFuncSetAttribute((const void*)k_gemm<MF, WM, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipFuncSetAttribute((const void*)k_gemm<MF, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int pairs = a.tiles * a.splits;
   const int grid = (pairs + 7) / 8 * 8 * a.mblocks;
-  k_gemm<MF, WM, EPI, P><<<grid, 256 * WM, lds, s>>>(a);
+  k_gemm<MF, EPI, P><<<grid, 256, lds, s>>>(a);
   return hipGetLastError();
 }
 
 template <int EPI, bool P>
 static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 32) return launch_mf<1, 1, EPI, P>(a, s);
-  if (a.M <= 64) return launch_mf<2, 1, EPI, P>(a, s);
-  if (a.M <= 128 || gemm_variant() != 1) return launch_mf<4, 1, EPI, P>(a, s);
-  return launch_mf<4, 2, EPI, P>(a, s);
+  if (a.M <= 32) return launch_mf<1, EPI, P>(a, s);
+  if (a.M <= 64) return launch_mf<2, EPI, P>(a, s);
+  return launch_mf<4, EPI, P>(a, s);
 }
 
 hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
