@@ -217,7 +217,7 @@ def main():
     ap.add_argument("--workload", default="llama70b_stack80")
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--mode", choices=["streamed", "resident"], default="streamed")
-    ap.add_argument("--copy", choices=["background", "burst", "memcpy"], default="background")
+    ap.add_argument("--copy", choices=["background", "burst", "memcpy", "sdma"], default="background")
     ap.add_argument("--pooling", choices=["layer", "ffn"], default="layer",
                     help="stage whole layers, or only their FFN part (attention weights read in place)")
     ap.add_argument("--ranks", type=int, default=0, help="pooling ranks d: layers l with l %% d == rank are owned")
@@ -329,6 +329,8 @@ def main():
         flags |= sidp.SIDP_COPY_MEMCPY
     elif args.copy == "burst":
         flags |= sidp.SIDP_COPY_BURST
+    elif args.copy == "sdma":
+        flags |= sidp.SIDP_COPY_SDMA
 
     dec.set_pooling(sidp.SIDP_POOL_FFN if args.pooling == "ffn" else sidp.SIDP_POOL_LAYER, args.ranks, args.rank)
     for i in range(args.warmup):

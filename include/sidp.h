@@ -55,6 +55,8 @@ extern "C" {
 #define SIDP_STREAMED      0x1  /* layers stream through the 2-slot cache ring */
 #define SIDP_COPY_MEMCPY   0x2  /* slot fills by hipMemcpyAsync                                  */
 #define SIDP_COPY_BURST    0x4  /* slot fills by a full-grid copy kernel                         */
+#define SIDP_COPY_SDMA     0x8  /* slot fills by hipMemcpyAsync of kind DeviceToDeviceNoCU: the  */
+                                /* DMA engines, no compute units                                 */
                                 /* default: a background fill kernel sized to run beside compute */
 #define SIDP_DEBUG_POISON  0x10 /* before each fill, write NaN bytes over the slot */
 #define SIDP_DEBUG_DELAY   0x20 /* before each fill, spin ~200 us on the copy stream */
@@ -178,7 +180,7 @@ int sidp_kv_attach(sidp_handle *h, void *k_cache, void *v_cache, int32_t num_phy
  *               new token's k, v are written at that position and attention
  *               covers positions[b] + 1 keys. The caller advances positions.
  *  block_tables device int32 [batch, max_blocks_per_seq] (from sidp_kv_alloc).
- *  flags        SIDP_RESIDENT or SIDP_STREAMED, optionally | SIDP_COPY_MEMCPY
+ *  flags        SIDP_RESIDENT or SIDP_STREAMED, optionally | one SIDP_COPY_* engine
  *               and the SIDP_DEBUG_* bits.
  *  compute      stream for the layer kernels.
  *  copy         stream for slot fills (STREAMED only; must differ from compute).

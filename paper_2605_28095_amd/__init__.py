@@ -26,6 +26,7 @@ SIDP_RESIDENT = 0x0
 SIDP_STREAMED = 0x1
 SIDP_COPY_MEMCPY = 0x2
 SIDP_COPY_BURST = 0x4
+SIDP_COPY_SDMA = 0x8
 SIDP_DEBUG_POISON = 0x10
 SIDP_DEBUG_DELAY = 0x20
 SIDP_TIMING = 0x40

@@ -634,6 +634,7 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   if (hi <= lo) return hipSuccess;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
+  else if (flags & SIDP_COPY_SDMA) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDeviceNoCU, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
   else {
     const bool small = h->step_batch < kFillSmallBatch;

@@ -103,6 +103,7 @@ def test_streamed_equals_resident_bitexact(lib, batch):
                             ("streamed", lib.SIDP_STREAMED),
                             ("streamed_memcpy", lib.SIDP_STREAMED | lib.SIDP_COPY_MEMCPY),
                             ("streamed_burst", lib.SIDP_STREAMED | lib.SIDP_COPY_BURST),
+                            ("streamed_sdma", lib.SIDP_STREAMED | lib.SIDP_COPY_SDMA),
                             ("streamed_poison_delay", lib.SIDP_STREAMED | lib.SIDP_DEBUG_POISON | lib.SIDP_DEBUG_DELAY)]:
             st.reset()
             for s in range(2):
