@@ -1,12 +1,12 @@
 // Paged grouped-query decode attention on gfx950 (K4).
 //
 // Work is a list of items (sequence b, partition p, KV head g), a partition
-// being 1024 tokens. A planning kernel, run once per set of positions, lists
+// being 2048 tokens. A planning kernel, run once per set of positions, lists
 // the full partitions first and then each sequence's shorter last partition
 // by decreasing length; a persistent grid of 4-wave workgroups walks that
 // list in snake order (workgroup w takes items w, 2G - 1 - w, 2G + w, ...),
 // which keeps the workgroups' totals within about one short item of each
-// other. Within an item each wave owns 256 tokens, processed in chunks of
+// other. Within an item each wave owns 512 tokens, processed in chunks of
 // 32 tokens = two 16-token KV blocks, with the next chunk's K/V loads in
 // flight while the current one computes. The query heads of a KV group (up to
 // 16) ride in the MFMA's 16 columns, so every KV byte is read once for all of
@@ -25,8 +25,8 @@
 
 namespace sidp {
 
-constexpr int kPartTokens = 1024;
-constexpr int kWaveTokens = 256;
+constexpr int kPartTokens = 2048;
+constexpr int kWaveTokens = kPartTokens / 4;  // each of an item's four waves
 constexpr float kLog2e = 1.4426950408889634f;
 
 int attn_part_tokens() { return kPartTokens; }
@@ -39,7 +39,7 @@ size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq) {
 size_t attn_plan_bytes(int max_batch, int max_parts) { return (1 + (size_t)max_batch * max_parts) * sizeof(int32_t); }
 
 // The work list. plan[0] = number of (sequence, partition) entries; entry i is
-// plan[1 + i] = b | part << 16. Full 1024-token partitions come first, in
+// plan[1 + i] = b | part << 16. Full 2048-token partitions come first, in
 // (b, part) order; then the last, shorter partition of every sequence that
 // has one, by decreasing length and then increasing b (a bitonic sort in
 // LDS). Positions outside a sequence's block table give no entries and set

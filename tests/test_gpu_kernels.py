@@ -230,7 +230,7 @@ def _attn_oracle(cfg, ctx, tables, k, v, q, absv=False):
                      for b in range(len(ctx))])
 
 
-ATTN_SEQS = [1, 2, 15, 16, 17, 31, 32, 33, 100, 511, 512, 513, 1024, 1500, 2049, 4097]
+ATTN_SEQS = [1, 2, 15, 16, 17, 31, 32, 33, 100, 511, 512, 513, 1024, 1500, 2047, 2048, 2049, 4096, 4097]
 
 
 @pytest.mark.parametrize("name,q_scale", [("tiny_layer", 1.0), ("llama70b_layer", 1.0), ("llama70b_layer", 4.0)])
