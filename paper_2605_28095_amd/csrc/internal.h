@@ -30,6 +30,7 @@ struct LinearCall {
 };
 
 size_t packed_bytes(int n, int k);
+bool gemm_fits(int m, int n_cols_packed, int k);  // within the kernels' 32-bit buffer offsets
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus);
 size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus);
 hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s);

@@ -351,6 +351,13 @@ __global__ void k_splitk_reduce(GemmArgs a) {
 
 size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k, 64) * 2; }
 
+// The kernels address the packed weights and the activations through 32-bit
+// buffer offsets.
+bool gemm_fits(int m, int n_cols_packed, int k) {
+  constexpr size_t kLimit = (size_t)1 << 32;
+  return packed_bytes(n_cols_packed, k) < kLimit && (size_t)m * round_up(k, 64) * 2 < kLimit;
+}
+
 
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int NG = round_up(n_cols_packed, 64) / 64;
@@ -450,6 +457,7 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   a.bias = (const uint16_t*)c.bias;
   a.resid = c.residual;
   a.ws = c.ws;
+  if (!gemm_fits(c.m, ncols, c.k)) return hipErrorInvalidValue;
   if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
   const bool fuse_norm = c.norm_out && c.epilogue == SIDP_EPI_RESID && c.residual == c.out;
   if (c.norm_out && !fuse_norm) return hipErrorInvalidValue;

@@ -65,16 +65,23 @@ BlobLayout blob_layout(const sidp_config& c) {
 
 bool config_ok(const sidp_config* c) {
   if (!c) return false;
-  if (c->num_layers < 1 || c->hidden < 64 || c->hidden % 64) return false;
+  if (c->num_layers < 1 || c->hidden < 64 || c->hidden % 64 || c->hidden > (1 << 17)) return false;
   if (c->head_dim != 64 && c->head_dim != 128) return false;
   if (c->num_q_heads < 1 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads) return false;
+  if (c->num_q_heads > 1024 || c->num_layers > 4096) return false;
   if (c->num_q_heads / c->num_kv_heads > 16) return false;
-  if (c->ffn_dim < 16 || c->ffn_dim % 16) return false;
+  if (c->ffn_dim < 16 || c->ffn_dim % 16 || c->ffn_dim > (1 << 20)) return false;
   if (c->block_size != 16) return false;
   if (c->max_batch < 1 || c->max_batch > 4096) return false;
   if (c->max_seq_len < 1 || c->max_seq_len > (1 << 20)) return false;
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return false;
   if (c->qk_norm && !(c->qk_norm_eps > 0.f)) return false;
+  // every projection within the GEMM's 32-bit buffer offsets at the largest batch
+  const int QD = c->num_q_heads * c->head_dim;
+  if (!gemm_fits(c->max_batch, qkv_rows(*c), c->hidden) || !gemm_fits(c->max_batch, c->hidden, QD) ||
+      !gemm_fits(c->max_batch, 2 * round_up_i(c->ffn_dim, 32), c->hidden) ||
+      !gemm_fits(c->max_batch, c->hidden, c->ffn_dim))
+    return false;
   return true;
 }
 
@@ -870,23 +877,25 @@ size_t sidp_packed_bytes(int32_t n, int32_t k) {
 }
 
 int sidp_pack_linear(const void* w, int32_t n, int32_t k, void* packed, void* stream) {
-  if (!w || !packed || n < 1 || k < 1) return SIDP_EINVAL;
+  if (!w || !packed || n < 1 || k < 1 || n > (1 << 24) || k > (1 << 24)) return SIDP_EINVAL;
   return launch_pack_linear(w, n, k, packed, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
 }
 
 int sidp_pack_gate_up(const void* w_gate, const void* w_up, int32_t f, int32_t k, void* packed, void* stream) {
-  if (!w_gate || !w_up || !packed || f < 1 || k < 1) return SIDP_EINVAL;
+  if (!w_gate || !w_up || !packed || f < 1 || k < 1 || f > (1 << 24) || k > (1 << 24)) return SIDP_EINVAL;
   return launch_pack_gate_up(w_gate, w_up, f, k, packed, (hipStream_t)stream) == hipSuccess ? SIDP_OK : SIDP_EHIP;
 }
 
 int sidp_linear(sidp_handle* h, const void* x, int32_t m, int32_t k, const void* packed, int32_t n, int32_t epilogue,
                 const void* bias, const float* residual, void* out, void* stream) {
   if (!h || !x || !packed || !out || m < 1 || m > h->cfg.max_batch || k < 8 || k % 8 || n < 1) return SIDP_EINVAL;
+  if (k > (1 << 24) || n > (1 << 24)) return SIDP_EINVAL;
   if (h->poisoned) return SIDP_ESTATE;
   if (epilogue < SIDP_EPI_BF16 || epilogue > SIDP_EPI_SWIGLU) return SIDP_EINVAL;
   if (epilogue == SIDP_EPI_RESID && !residual) return SIDP_EINVAL;
   if (epilogue != SIDP_EPI_BF16 && bias) return SIDP_EINVAL;
   const int ncols = epilogue == SIDP_EPI_SWIGLU ? 2 * round_up_i(n, 32) : n;
+  if (!gemm_fits(m, ncols, k)) return SIDP_EINVAL;
   if (gemm_ws_bytes(m, ncols, k, h->num_cus) > h->ws_bytes) return SIDP_EINVAL;
   HIPCHK(h, launch_linear(linear_call(h, x, m, k, packed, n, epilogue, bias, residual, out), (hipStream_t)stream));
   h->last_compute = (hipStream_t)stream;

@@ -90,13 +90,18 @@ def test_config_validation_on_host():
     assert lb % 256 == 0
     assert 2 * synth.layer_param_count(cfg) <= lb < 2 * synth.layer_param_count(cfg) + 64 * 1024
     for field, bad in [("head_dim", 96), ("num_kv_heads", 7), ("block_size", 32), ("hidden", 100),
-                       ("ffn_dim", 20), ("max_batch", 0)]:
+                       ("ffn_dim", 20), ("max_batch", 0), ("hidden", 1 << 18), ("ffn_dim", 1 << 21)]:
         c = sidp.make_config(cfg, 256, 8192)
         setattr(c, field, bad)
         assert sidp.sidp_layer_bytes(c) == 0, field
     c = sidp.make_config(cfg, 256, 8192)
     c.num_q_heads = 64
     c.num_kv_heads = 2  # group of 32 query heads per KV head is not supported
+    assert sidp.sidp_layer_bytes(c) == 0
+    # each field in range, but the packed gate/up (2 * 2^20 x 2^15 bf16 = 128 GiB) would overflow
+    # the projections' 32-bit buffer offsets
+    c = sidp.make_config(cfg, 256, 8192)
+    c.hidden, c.ffn_dim = 1 << 15, 1 << 20
     assert sidp.sidp_layer_bytes(c) == 0
     assert sidp.sidp_kv_region_bytes(good, 10) == 10 * 8 * 16 * 128 * 2
     assert sidp.sidp_packed_bytes(688, 256) == 704 * 256 * 2

@@ -123,6 +123,10 @@ def test_linear_rejects_bad_arguments(lib, tiny_handle):
                         out.data_ptr(), None) == E  # k not a multiple of 8
     assert lib.raw_call("sidp_linear", tiny_handle, x.data_ptr(), 513, 256, p.data_ptr(), 64, 0, None, None,
                         out.data_ptr(), None) == E  # m beyond max_batch
+    # packed weights past the kernels' 32-bit buffer offsets (2^21 x 2^12 bf16 = 16 GiB): refused
+    # on the host before any launch (the buffers are never touched)
+    assert lib.raw_call("sidp_linear", tiny_handle, x.data_ptr(), 4, 1 << 12, p.data_ptr(), 1 << 21, 0, None, None,
+                        out.data_ptr(), None) == E
 
 
 # ------------------------------------------------------------------ RoPE + KV append
