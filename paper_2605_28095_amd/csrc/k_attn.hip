@@ -288,8 +288,13 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     it.seq = positions[it.b] + 1;
     it.nparts = (it.seq + kPartTokens - 1) / kPartTokens;
     it.bt = (cint32_t*)(a.block_tables + (int64_t)it.b * a.max_blocks);
-    it.tb = it.part * kPartTokens + wave * kWaveTokens;
-    it.te = min(it.tb + kWaveTokens, it.seq);
+    // the partition's tokens split evenly over the four waves in whole 32-token
+    // chunks (kWaveTokens each for a full partition), so a sequence's shorter
+    // last partition keeps all four waves loading
+    const int len = min(it.seq - it.part * kPartTokens, kPartTokens);
+    const int share = ((len + 3) / 4 + 31) / 32 * 32;
+    it.tb = it.part * kPartTokens + wave * share;
+    it.te = min(it.tb + share, it.seq);
   };
   // the r-th item of this workgroup in snake order over the sorted list
   auto item_of = [&](int r) {
