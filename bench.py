@@ -237,9 +237,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU's share of the decode step; runs on more than one GPU are not "
-              "part of this build (see the sharding notes: each GPU would run this same step on its own "
-              "batch and pull non-owned layers over xGMI).", file=sys.stderr)
+        print("bench.py measures one GPU's share of the decode step; runs on several GPUs are not "
+              "implemented (each GPU would run this same step on its own batch and pull the layers it "
+              "does not own over xGMI).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
