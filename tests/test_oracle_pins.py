@@ -30,7 +30,7 @@ def test_bf16_roundtrip_and_rne():
     vals = od.bf16_bits_to_f64(bits)
     finite = ~np.isnan(vals)
     assert np.array_equal(od.f64_to_bf16_bits(vals[finite]), bits[finite])
-    # torch's own float32 -> bfloat16 conversion (round to nearest even) as the judge.
+    # torch's own float32 -> bfloat16 conversion (round to nearest even) as the reference.
     x = np.random.default_rng(0).standard_normal(100_000).astype(np.float32) * 37.0
     x = np.concatenate([x, np.float32([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -8, 65504.0, 3.0e38])])
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
