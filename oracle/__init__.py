@@ -22,6 +22,9 @@ What it computes (SiDP, arXiv 2605.28095):
     of those operations.
   * kvalloc.py holds the paged-KV block allocation (a seeded permutation of the
     physical blocks) and the token -> slot mapping.
+  * §4.3 "Consistent mode switching": orchestrator.py holds the group-wide
+    choice between WaS and CaS from the engines' active sequences, B_th and
+    hysteresis.
 
 The per-op equations (RMSNorm, rotate-half RoPE, grouped-query attention,
 SwiGLU, per-head QK RMSNorm, QKV bias) are not printed in the paper; they are

@@ -443,3 +443,61 @@ def test_bf16_mode_close_to_exact_mode():
     rel = np.max(np.abs(a - b), axis=1) / np.max(np.abs(b), axis=1)
     assert rel.max() < 5e-3
     assert np.any(a != b)
+
+
+# ---------------------------------------------------------------- mode switching (§4.3)
+
+def test_mode_schedule_switches_after_a_persistent_drop():
+    from oracle.orchestrator import WAS, CAS, mode_schedule
+    b_th, h, W = 64, 0.5, 4
+    # above the threshold throughout: never leaves WaS
+    assert mode_schedule([[200, 100]] * 20, b_th, h, W) == [WAS] * 20
+    # the effective batch drops below B_th from iteration 5 on: the first CaS iteration is 5 + W
+    trace = [[100, 100]] * 5 + [[40, 40]] * 15
+    modes = mode_schedule(trace, b_th, h, W)
+    assert modes.index(CAS) == 5 + W and all(m == CAS for m in modes[5 + W:])
+    # dips shorter than the window never switch
+    trace = ([[100, 100]] * 3 + [[10, 10]] * (W - 1)) * 5
+    assert mode_schedule(trace, b_th, h, W) == [WAS] * len(trace)
+    # the effective batch is the mean over all engines, idle ones (0 active) included
+    trace = [[100, 100, 0, 0]] * 10  # mean 50 < 64 although two engines run 100 rows
+    assert mode_schedule(trace, b_th, h, W)[W] == CAS
+
+
+def test_mode_schedule_hysteresis():
+    from oracle.orchestrator import WAS, CAS, mode_schedule
+    b_th, h, W = 64, 0.5, 3
+    down = [[10, 10]] * W           # into CaS
+    band = [[80, 80]] * 10          # above B_th but below B_th * 1.5 = 96: stays in CaS
+    up = [[100, 100]] * (W + 2)     # at least 96: back to WaS after W iterations
+    modes = mode_schedule(down + band + up, b_th, h, W)
+    assert modes[W:W + 10] == [CAS] * 10
+    k = W + 10  # first iteration at or above B_th * (1 + h); WaS from k + W on
+    assert modes[k:k + W] == [CAS] * W and modes[k + W:] == [WAS] * 2
+    # exactly at the upper edge counts as "at least"
+    assert mode_schedule(down + [[96, 96]] * (W + 1), b_th, h, W)[2 * W] == WAS
+
+
+def test_mode_schedule_invariants_on_random_traces():
+    """On random tails: every switch is preceded by exactly the window of
+    qualifying iterations in the old mode, and successive switches are at
+    least a window apart (no flapping)."""
+    from oracle.orchestrator import WAS, CAS, effective_batch, mode_schedule
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        n, T, W = int(rng.integers(1, 9)), int(rng.integers(5, 80)), int(rng.integers(1, 6))
+        b_th, h = float(rng.integers(8, 128)), float(rng.uniform(0, 1))
+        trace = [list(map(int, rng.integers(0, 256, n))) for _ in range(T)]
+        modes = mode_schedule(trace, b_th, h, W)
+        assert modes[0] == WAS
+        last = None
+        for t in range(1, T):
+            if modes[t] != modes[t - 1]:
+                window = [effective_batch(trace[s]) for s in range(t - W, t)]
+                assert t - W >= 0 and all(m == modes[t - 1] for m in modes[t - W:t])
+                if modes[t] == CAS:
+                    assert all(b < b_th for b in window)
+                else:
+                    assert all(b >= b_th * (1 + h) for b in window)
+                assert last is None or t - last >= W
+                last = t
