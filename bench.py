@@ -202,11 +202,65 @@ def bth_leg(dec, hidden, pos, bt, stage_bytes, L, batches, stream, reps=3):
              "xgmi_1_link_modeled": stage_bytes / (XGMI_LINK_GBS * 1e9) * 1e3}
     del src, dst
     bth = {k: next((b for b, t in zip(batches, layer_ms) if t >= f), None) for k, f in fetch.items()}
+
+    def crossing(f):  # the batch where T(B) reaches f, linear between profiled points
+        if layer_ms[0] >= f:
+            return float(batches[0])
+        for (b0, t0), (b1, t1) in zip(zip(batches, layer_ms), zip(batches[1:], layer_ms[1:])):
+            if t0 < f <= t1:
+                return b0 + (b1 - b0) * (f - t0) / (t1 - t0)
+        return None
+    bth_interp = {k: (round(crossing(f), 1) if crossing(f) is not None else None) for k, f in fetch.items()}
     log("B_th profile: " + ", ".join(f"B={b}: {t:.3f} ms/layer" for b, t in zip(batches, layer_ms)))
     log("fetch per layer: " + ", ".join(f"{k} {v:.3f} ms" for k, v in fetch.items()) + f"; B_th {bth}")
     return {"batches": batches, "layer_ms": [round(t, 4) for t in layer_ms],
             "fetch_ms": {k: round(v, 4) for k, v in fetch.items()}, "staged_bytes": stage_bytes, "b_th": bth,
+            "b_th_interp": bth_interp,
             "note": "B_th = smallest profiled batch whose resident per-layer time covers the fetch; null: none"}
+
+
+def tail_trace(engines, batch, requests, max_len, seed=0):
+    """Active sequences per engine and iteration of a synthetic offline job:
+    each of `engines` engines serves `requests` requests with output lengths
+    U[1, max_len] through `batch` continuous-batching lanes, each waiting
+    request taking the first lane to free up, so the batch stays full until
+    the queue runs dry and then decays. Returns an int64 array [T, engines]."""
+    import heapq
+    import numpy as np
+    rng = np.random.default_rng([seed, 4242])
+    lane_ends = []
+    for _ in range(engines):
+        lanes = [0] * batch
+        for n in rng.integers(1, max_len + 1, requests).tolist():
+            heapq.heapreplace(lanes, lanes[0] + n)
+        lane_ends.append(np.sort(np.array(lanes, np.int64)))
+    T = int(max(e[-1] for e in lane_ends))
+    # active lanes of engine e at iteration t: lanes whose work ends after t
+    return np.stack([batch - np.searchsorted(e, np.arange(T), side="right") for e in lane_ends], axis=1)
+
+
+def tail_leg(b_th, engines=8, batch=256, requests=4096, max_len=2048, window=64, hysteresis=0.5, seed=0):
+    """§4.3 mode switching over the tail of a synthetic offline job
+    (tail_trace): the library's mode choice (sidp_mode_update) runs on every
+    iteration's per-engine active counts with each B_th estimate."""
+    import paper_2605_28095_amd as sidp
+    active = tail_trace(engines, batch, requests, max_len, seed)
+    T = active.shape[0]
+    out = {"engines": engines, "batch": batch, "requests_per_engine": requests, "max_output_len": max_len,
+           "window": window, "hysteresis": hysteresis, "iterations": T, "by_b_th": {}}
+    for name, bt in b_th.items():
+        if bt is None:
+            continue
+        modes = sidp.mode_schedule(float(bt), hysteresis, window, active.tolist())
+        switches = int(sum(1 for a, b in zip(modes, modes[1:]) if a != b))
+        first_cas = next((t for t, m in enumerate(modes) if m == sidp.SIDP_MODE_CAS), None)
+        out["by_b_th"][name] = {
+            "b_th": bt, "was_fraction": round(modes.count(sidp.SIDP_MODE_WAS) / T, 4), "switches": switches,
+            "first_cas_iteration": first_cas,
+            "mean_active_at_switch": (round(float(active[first_cas].mean()), 1) if first_cas is not None else None)}
+        log(f"tail ({name}, B_th {bt}): {100 * modes.count(sidp.SIDP_MODE_WAS) / T:.1f}% of {T} iterations in WaS, "
+            f"{switches} switch(es), CaS from iteration {first_cas}")
+    return out
 
 
 def main():
@@ -225,6 +279,9 @@ def main():
     ap.add_argument("--cas", type=int, default=0,
                     help="also time the owner-side CaS FFN over this many replicas (0: skip)")
     ap.add_argument("--cas-rows", type=int, default=16, help="rows per CaS replica")
+    ap.add_argument("--tail", action="store_true",
+                    help="also run the WaS/CaS mode choice over a synthetic job tail with the profiled B_th "
+                         "(implies --bth)")
     ap.add_argument("--bth", action="store_true",
                     help="also profile B_th: the smallest batch whose layer time covers one layer's weight fetch")
     ap.add_argument("--seed", type=int, default=0)
@@ -427,7 +484,7 @@ def main():
 
     cas = cas_leg(dec, cfg, args.cas, args.cas_rows, compute) if args.cas > 0 else None
     bth = None
-    if args.bth:
+    if args.bth or args.tail:
         batches = [b for b in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512) if b <= B]
         bth = bth_leg(dec, hidden, pos, bt, fill_bytes, L, batches, compute)
 
@@ -454,6 +511,8 @@ def main():
         out["cas"] = cas
     if bth:
         out["bth"] = bth
+    if args.tail:
+        out["tail"] = tail_leg(bth["b_th_interp"])
     print(json.dumps(out), flush=True)
     dec.close()
 

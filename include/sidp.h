@@ -273,6 +273,35 @@ int sidp_cas_ffn(sidp_handle *h, int32_t layer, int32_t n_replicas, const void *
  * arguments are bad. */
 int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, int32_t *ops, int32_t *n_ops);
 
+/* ---- WaS / CaS mode choice (host only; §4.3 "Consistent mode switching") ----
+ * The job orchestrator picks one mode for every engine of the group, so all
+ * ranks agree on each layer's communication pattern. WaS stays while the
+ * effective batch (mean active sequences over the group's engines, idle ones
+ * counted as 0) is at least b_th, the smallest batch whose forward time hides
+ * a layer's weight fetch (from offline profiling, e.g. bench.py --bth); after
+ * `window` consecutive iterations below b_th the group switches to CaS, and
+ * back to WaS only after `window` consecutive iterations at or above
+ * b_th * (1 + hysteresis). A decision applies from the next iteration.
+ * sidp_mode_update takes iteration t's per-engine active counts
+ * (`active`, host int32 [n_engines], each >= 0), advances `state` (caller
+ * owned; all zeros = WaS, the job's start) and writes the mode iteration t + 1
+ * runs in to *mode. SIDP_EINVAL for null pointers, n_engines < 1, a negative
+ * count, b_th <= 0 or NaN, hysteresis < 0, window < 1 or a state whose mode is
+ * neither value; the state is then unchanged. */
+#define SIDP_MODE_WAS 0
+#define SIDP_MODE_CAS 1
+typedef struct {
+  float b_th;
+  float hysteresis;
+  int32_t window;
+} sidp_mode_policy;
+typedef struct {
+  int32_t mode; /* SIDP_MODE_WAS or SIDP_MODE_CAS */
+  int32_t run;  /* consecutive iterations the switching condition has held */
+} sidp_mode_state;
+int sidp_mode_update(const sidp_mode_policy *policy, sidp_mode_state *state, int32_t n_engines, const int32_t *active,
+                     int32_t *mode);
+
 /* ---- single kernels, for parity checks and reuse ----
  * All enqueue on `stream` and return immediately. */
 

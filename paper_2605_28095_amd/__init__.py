@@ -49,7 +49,7 @@ EXPORTED = [
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
-    "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select",
+    "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select", "sidp_mode_update",
 ]
 
 SIDP_CAS_MAX_REPLICAS = 16
@@ -66,6 +66,18 @@ class sidp_config(ctypes.Structure):
         "num_layers", "hidden", "num_q_heads", "num_kv_heads", "head_dim", "ffn_dim", "qkv_bias", "qk_norm",
         "block_size", "max_batch", "max_seq_len")] + [
         ("rms_eps", ctypes.c_float), ("qk_norm_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+
+
+class sidp_mode_policy(ctypes.Structure):
+    _fields_ = [("b_th", ctypes.c_float), ("hysteresis", ctypes.c_float), ("window", ctypes.c_int32)]
+
+
+class sidp_mode_state(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("run", ctypes.c_int32)]
+
+
+SIDP_MODE_WAS = 0
+SIDP_MODE_CAS = 1
 
 
 class sidp_layer_weights(ctypes.Structure):
@@ -114,6 +126,8 @@ _sigs = {
     "sidp_attention": (ctypes.c_int, [_P, _P, _I, _P, _P, _I, _I, _P, _P]),
     "sidp_copy": (ctypes.c_int, [_P, _P, _Z, _I, _P]),
     "sidp_timing_collect": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), _PI]),
+    "sidp_mode_update": (ctypes.c_int, [ctypes.POINTER(sidp_mode_policy), ctypes.POINTER(sidp_mode_state), _I, _PI,
+                                        _PI]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -225,6 +239,28 @@ def sidp_plan(num_layers, steps, ranks=0, rank=0):
     n = ctypes.c_int32(cap)
     _check(_lib.sidp_plan(num_layers, steps, ranks, rank, buf, ctypes.byref(n)), "sidp_plan")
     return [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n.value)]
+
+
+def sidp_mode_update(policy, state, active):
+    """Advances `state` (a sidp_mode_state) by one iteration whose engines have
+    `active` sequences each; returns the mode of the next iteration."""
+    arr = (ctypes.c_int32 * len(active))(*[int(a) for a in active])
+    mode = ctypes.c_int32(-1)
+    _check(_lib.sidp_mode_update(ctypes.byref(policy), ctypes.byref(state), len(active), arr, ctypes.byref(mode)),
+           "sidp_mode_update")
+    return mode.value
+
+
+def mode_schedule(b_th, hysteresis, window, batches):
+    """The mode of every iteration of a trace (list of per-engine active
+    counts per iteration), the job starting in WaS."""
+    pol = sidp_mode_policy(b_th, hysteresis, window)
+    st = sidp_mode_state(SIDP_MODE_WAS, 0)
+    modes, mode = [], SIDP_MODE_WAS
+    for active in batches:
+        modes.append(mode)
+        mode = sidp_mode_update(pol, st, active)
+    return modes
 
 
 def sidp_set_pooling(h, mode, ranks=0, rank=0):

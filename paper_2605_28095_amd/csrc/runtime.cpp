@@ -864,6 +864,29 @@ int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, in
   return SIDP_OK;
 }
 
+// ---------------------------------------------------------------- mode choice
+
+int sidp_mode_update(const sidp_mode_policy* p, sidp_mode_state* st, int32_t n_engines, const int32_t* active,
+                     int32_t* mode) {
+  if (!p || !st || !active || !mode || n_engines < 1) return SIDP_EINVAL;
+  if (!(p->b_th > 0.f) || !(p->hysteresis >= 0.f) || p->window < 1) return SIDP_EINVAL;
+  if (st->mode != SIDP_MODE_WAS && st->mode != SIDP_MODE_CAS) return SIDP_EINVAL;
+  double sum = 0.0;
+  for (int32_t i = 0; i < n_engines; i++) {
+    if (active[i] < 0) return SIDP_EINVAL;
+    sum += active[i];
+  }
+  const double b = sum / n_engines;
+  const bool cond = st->mode == SIDP_MODE_WAS ? b < (double)p->b_th : b >= (double)p->b_th * (1.0 + p->hysteresis);
+  st->run = cond ? st->run + 1 : 0;
+  if (st->run >= p->window) {
+    st->mode = st->mode == SIDP_MODE_WAS ? SIDP_MODE_CAS : SIDP_MODE_WAS;
+    st->run = 0;
+  }
+  *mode = st->mode;
+  return SIDP_OK;
+}
+
 // ---------------------------------------------------------------- single kernels
 
 int sidp_rmsnorm(const float* x, const void* gain, float eps, void* out, int32_t rows, int32_t n, void* stream) {

@@ -136,3 +136,34 @@ def test_key_block_layout_helpers():
             g, t = lane // 16, lane % 16
             assert torch.equal(run[lane], k[1, 0, t, 32 * kk + 8 * g:32 * kk + 8 * g + 8])
     assert torch.equal(sidp.k_blocks_from_lib(kl), k)
+
+
+def test_mode_update_matches_oracle():
+    """The library's WaS/CaS choice equals the oracle's on random job tails
+    (thresholds drawn as float32 values, which both sides then use exactly)."""
+    import paper_2605_28095_amd as sidp
+    from oracle.orchestrator import mode_schedule
+    rng = np.random.default_rng(11)
+    for _ in range(300):
+        n, T, W = int(rng.integers(1, 9)), int(rng.integers(1, 120)), int(rng.integers(1, 7))
+        b_th = float(np.float32(rng.uniform(1, 200)))
+        h = float(np.float32(rng.choice([0.0, 0.25, 0.5, float(rng.uniform(0, 1))])))
+        # a shrinking tail with noise, sometimes recovering
+        base = np.maximum(0, 256 - np.cumsum(rng.integers(0, 12, T)))
+        trace = [list(map(int, np.clip(base[t] + rng.integers(-20, 21, n), 0, None))) for t in range(T)]
+        if rng.random() < 0.3:
+            trace = trace[::-1]
+        assert sidp.mode_schedule(b_th, h, W, trace) == mode_schedule(trace, b_th, h, W)
+
+
+def test_mode_update_rejects_bad_arguments():
+    import paper_2605_28095_amd as sidp
+    st = sidp.sidp_mode_state(0, 0)
+    for pol, active in [(sidp.sidp_mode_policy(0.0, 0.5, 3), [4]), (sidp.sidp_mode_policy(8.0, -0.1, 3), [4]),
+                        (sidp.sidp_mode_policy(8.0, 0.5, 0), [4]), (sidp.sidp_mode_policy(8.0, 0.5, 3), [4, -1])]:
+        with pytest.raises(sidp.SidpError) as e:
+            sidp.sidp_mode_update(pol, st, active)
+        assert e.value.code == sidp.SIDP_EINVAL
+        assert (st.mode, st.run) == (0, 0)  # unchanged
+    with pytest.raises(sidp.SidpError):
+        sidp.sidp_mode_update(sidp.sidp_mode_policy(8.0, 0.5, 3), st, [])

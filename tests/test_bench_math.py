@@ -50,3 +50,34 @@ def test_attended_tokens_follow_the_context_recipe():
     ctx = synth.context_lengths(cfg, 0, 256)
     assert ctx.min() >= 1024 and ctx.max() <= 8192
     assert abs(ctx.mean() - (1024 + 8192) / 2) < 200  # uniform over [1024, 8192]
+
+
+def test_tail_trace_is_a_draining_continuous_batch():
+    a = bench.tail_trace(engines=3, batch=16, requests=200, max_len=64, seed=1)
+    T, E = a.shape
+    assert E == 3 and a[0].tolist() == [16] * 3
+    assert (np.diff(a, axis=0) <= 0).all() and (a >= 0).all()  # nobody joins once the queue is dry
+    assert a[-1].max() >= 1  # the last iteration still has work
+    # every engine's total work (lane-iterations) is the sum of its requests' lengths
+    rng = np.random.default_rng([1, 4242])
+    for e in range(E):
+        assert a[:, e].sum() == rng.integers(1, 65, 200).sum()
+    # greedy assignment: an engine stays full until its queue is empty, so its batch
+    # decays over at most one maximum request length
+    for e in range(E):
+        full_until = int(np.argmax(a[:, e] < 16))
+        drained = int(np.argmax(a[:, e] == 0)) if (a[:, e] == 0).any() else T
+        assert drained - full_until <= 64
+
+
+def test_tail_leg_mode_choice_matches_the_oracle():
+    from oracle import orchestrator
+    bt, W, h = 6.0, 8, 0.5
+    a = bench.tail_trace(engines=3, batch=16, requests=200, max_len=64, seed=1)
+    want = orchestrator.mode_schedule(a.tolist(), bt, h, W)
+    r = bench.tail_leg({"x": bt}, engines=3, batch=16, requests=200, max_len=64, window=W, hysteresis=h, seed=1)
+    got = r["by_b_th"]["x"]
+    assert r["iterations"] == len(want)
+    assert got["was_fraction"] == round(want.count(orchestrator.WAS) / len(want), 4)
+    assert got["first_cas_iteration"] == want.index(orchestrator.CAS)
+    assert got["switches"] == sum(1 for p, q in zip(want, want[1:]) if p != q) == 1
