@@ -247,9 +247,10 @@ def tail_leg(b_th, engines=8, batch=256, requests=4096, max_len=2048, window=64,
     active = tail_trace(engines, batch, requests, max_len, seed)
     T = active.shape[0]
     out = {"engines": engines, "batch": batch, "requests_per_engine": requests, "max_output_len": max_len,
-           "window": window, "hysteresis": hysteresis, "iterations": T, "by_b_th": {}}
+           "window": window, "hysteresis": hysteresis, "iterations": T, "by_b_th": {}, "skipped": {}}
     for name, bt in b_th.items():
         if bt is None:
+            out["skipped"][name] = "no profiled batch hides this fetch: the job would run in CaS throughout"
             continue
         modes = sidp.mode_schedule(float(bt), hysteresis, window, active.tolist())
         switches = int(sum(1 for a, b in zip(modes, modes[1:]) if a != b))

@@ -247,6 +247,20 @@ def test_attention_parity(lib, name, q_scale):
     assert_bf16_within_ulp(got, want, what="attention", abs_tol=2.0 ** -12 * pv)
 
 
+def test_attention_longest_context(lib):
+    """A sequence at the longest context a handle accepts (2^20 positions:
+    512 partitions merged by the combine kernel), ragged in its last block,
+    beside a short and a two-partition one."""
+    cfg = synth.get_config("tiny_layer")
+    seqs = [(1 << 20) - 21, 5, 2049]
+    ctx, tables, nblk, k, v, q, maxb = _attn_setup(lib, cfg, seqs, nblk_extra=3)
+    assert maxb * 16 + 16 == 1 << 20  # the handle's max_seq_len at its limit
+    got = _attn_run(lib, cfg, ctx, tables, nblk, k, v, q, maxb)
+    want = _attn_oracle(cfg, ctx, tables, k, v, q)
+    pv = _attn_oracle(cfg, ctx, tables, k, v, q, absv=True)
+    assert_bf16_within_ulp(got, want, what="attention, longest context", abs_tol=2.0 ** -12 * pv)
+
+
 def test_attention_closed_forms_on_gpu(lib):
     cfg = synth.get_config("llama70b_layer")
     # one cached token: the output is exactly that token's V row

@@ -282,6 +282,25 @@ def test_full_size_layer_batch512_sampled_rows(lib):
         st.close()
 
 
+def test_full_size_layer_max_batch_sampled_rows(lib):
+    """The 70B layer at the largest batch a handle accepts (4096 rows): 32 row
+    blocks per projection column tile, a 4096-entry attention work list
+    (the plan's LDS at its largest), short ragged contexts; rows from the
+    first, a middle and the last row block recomputed by the oracle."""
+    cfg = synth.get_config("llama70b_layer", batch=4096, ctx_lo=0, ctx_hi=300)
+    st = Stack(cfg, keep_weights=False)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        rows = [0, 2049, 4095]
+        got = st.hidden.double().cpu().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        e = row_rel_err(got, want)
+        assert e.max() <= TIGHT, e
+    finally:
+        st.close()
+
+
 @pytest.mark.slow
 def test_qwen25_stack8_streamed_sampled_rows(lib):
     cfg = synth.get_config("qwen25_72b_stack8")
