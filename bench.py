@@ -239,11 +239,13 @@ def tail_trace(engines, batch, requests, max_len, seed=0):
     return np.stack([batch - np.searchsorted(e, np.arange(T), side="right") for e in lane_ends], axis=1)
 
 
-def tail_leg(b_th, engines=8, batch=256, requests=4096, max_len=2048, window=64, hysteresis=0.5, seed=0):
+def tail_leg(b_th, engines=8, batch=256, requests=None, max_len=2048, window=64, hysteresis=0.5, seed=0):
     """§4.3 mode switching over the tail of a synthetic offline job
-    (tail_trace): the library's mode choice (sidp_mode_update) runs on every
-    iteration's per-engine active counts with each B_th estimate."""
+    (tail_trace; by default 16 requests per lane): the library's mode choice
+    (sidp_mode_update) runs on every iteration's per-engine active counts with
+    each B_th estimate."""
     import paper_2605_28095_amd as sidp
+    requests = requests or 16 * batch
     active = tail_trace(engines, batch, requests, max_len, seed)
     T = active.shape[0]
     out = {"engines": engines, "batch": batch, "requests_per_engine": requests, "max_output_len": max_len,
@@ -281,8 +283,8 @@ def main():
                     help="also time the owner-side CaS FFN over this many replicas (0: skip)")
     ap.add_argument("--cas-rows", type=int, default=16, help="rows per CaS replica")
     ap.add_argument("--tail", action="store_true",
-                    help="also run the WaS/CaS mode choice over a synthetic job tail with the profiled B_th "
-                         "(implies --bth)")
+                    help="also run the WaS/CaS mode choice over a synthetic job tail with the profiled B_th, "
+                         "engines of --batch lanes (implies --bth)")
     ap.add_argument("--bth", action="store_true",
                     help="also profile B_th: the smallest batch whose layer time covers one layer's weight fetch")
     ap.add_argument("--seed", type=int, default=0)
@@ -513,7 +515,7 @@ def main():
     if bth:
         out["bth"] = bth
     if args.tail:
-        out["tail"] = tail_leg(bth["b_th_interp"])
+        out["tail"] = tail_leg(bth["b_th_interp"], batch=B)
     print(json.dumps(out), flush=True)
     dec.close()
 
