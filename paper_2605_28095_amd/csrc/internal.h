@@ -85,14 +85,16 @@ struct AttnCall {
   KvView kv;
   int region;
   uint16_t* out;      // [B][Hq][D]
-  float* part;        // partials [B][Hq][max_parts][D + 4]: o[D], m, l, 2 pad
+  float* part;        // partials [B][Hkv][max_parts] records of Hq/Hkv*D + 32 floats: o[Hq/Hkv][D], (m, l) per head, pad
   int max_parts;
   uint32_t* err;
   int num_cus;
   int32_t* plan;      // work list written by launch_attn_plan: [0] count, [1 + i] b | part << 16
+  int part_tokens;    // partition length, set by launch_attention (attn_part_tokens_for)
 };
-int attn_part_tokens();
-size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq);
+int attn_part_tokens();  // the partition quantum (and shortest partition)
+int attn_part_tokens_for(int batch, int hkv, int max_tokens, int num_cus);
+size_t attn_ws_bytes(int max_batch, int hq, int hkv, int d, int max_seq);
 size_t attn_plan_bytes(int max_batch, int max_parts);
 // Builds the work list from positions; needed once per set of positions (a
 // decode step shares it across its layers). Reads positions, batch,

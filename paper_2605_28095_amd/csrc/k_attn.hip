@@ -1,14 +1,16 @@
 // Paged grouped-query decode attention on gfx950 (K4).
 //
-// Work is a list of items (sequence b, partition p, KV head g), a partition
-// being 2048 tokens. A planning kernel, run once per set of positions, lists
-// the full partitions first and then each sequence's shorter last partition
-// by decreasing length; a persistent grid of 4-wave workgroups walks that
-// list in snake order (workgroup w takes items w, 2G - 1 - w, 2G + w, ...),
-// which keeps the workgroups' totals within about one short item of each
-// other. Within an item each wave owns 512 tokens, processed in chunks of
-// 32 tokens = two 16-token KV blocks, with the next chunk's K/V loads in
-// flight while the current one computes. The query heads of a KV group (up to
+// Work is a list of items (sequence b, partition p, KV head g). The partition
+// length is chosen per launch (attn_part_tokens_for): whole sequences when
+// the batch alone gives every workgroup several items, else as many
+// 2048-token multiples as that takes. A planning kernel, run once per set of
+// positions, lists the full partitions first and then each sequence's shorter
+// last partition by decreasing length; a persistent grid of 4-wave workgroups
+// walks that list in snake order (workgroup w takes items w, 2G - 1 - w,
+// 2G + w, ...), which keeps the workgroups' totals within about one short item
+// of each other. Within an item each wave owns a quarter of the tokens,
+// processed in chunks of 32 tokens = two 16-token KV blocks, with the next
+// chunk's K/V loads in flight while the current one computes. The query heads of a KV group (up to
 // 16) ride in the MFMA's 16 columns, so every KV byte is read once for all of
 // them:
 //   S^T[token][head] = K[token][:] . Q^T[:][head]   (v_mfma_f32_16x16x32_bf16)
@@ -25,15 +27,36 @@
 
 namespace sidp {
 
-constexpr int kPartTokens = 2048;
-constexpr int kWaveTokens = kPartTokens / 4;  // each of an item's four waves
+constexpr int kPartQuantum = 2048;  // partition lengths are multiples of this
 constexpr float kLog2e = 1.4426950408889634f;
 
-int attn_part_tokens() { return kPartTokens; }
+int attn_part_tokens() { return kPartQuantum; }
 
-size_t attn_ws_bytes(int max_batch, int hq, int d, int max_seq) {
-  const int parts = (max_seq + kPartTokens - 1) / kPartTokens;
-  return (size_t)max_batch * hq * parts * (d + 4) * sizeof(float);
+// Partition length of a launch. Whole sequences (no partial records and no
+// combine) when batch x Hkv items already give each of the 2 x CUs persistent
+// workgroups four of them; otherwise the longest sequence the block tables
+// allow is cut into as many pieces as that takes, rounded up to the quantum.
+// Partials written for a later merge cost HBM writes beside the KV stream
+// that slow it by more than their bytes, so fewer partitions are better as
+// long as the workgroups stay balanced.
+int attn_part_tokens_for(int batch, int hkv, int max_tokens, int num_cus) {
+  const int64_t items = (int64_t)std::max(batch, 1) * std::max(hkv, 1);
+  const int64_t want = 4 * 2 * (int64_t)std::max(num_cus, 1);
+  const int64_t pieces = items >= want ? 1 : (want + items - 1) / items;
+  const int64_t p = (max_tokens + pieces - 1) / pieces;
+  return (int)std::max<int64_t>(kPartQuantum, (p + kPartQuantum - 1) / kPartQuantum * kPartQuantum);
+}
+
+// One partial record per (sequence, KV head, partition): the group's outputs
+// o[group][D], then a 128-byte line with (m, l) of each query head, zero
+// padded. Records are whole cache lines (group * D is a multiple of 64), so
+// every write of a record covers whole lines: HBM has no write mask, and a
+// partly written line costs the memory controller a read-modify-write.
+static __host__ __device__ inline int attn_rec_floats(int group, int d) { return group * d + 32; }
+
+size_t attn_ws_bytes(int max_batch, int hq, int hkv, int d, int max_seq) {
+  const int parts = (max_seq + kPartQuantum - 1) / kPartQuantum;
+  return (size_t)max_batch * hkv * parts * attn_rec_floats(hq / hkv, d) * sizeof(float);
 }
 
 size_t attn_plan_bytes(int max_batch, int max_parts) { return (1 + (size_t)max_batch * max_parts) * sizeof(int32_t); }
@@ -45,7 +68,7 @@ size_t attn_plan_bytes(int max_batch, int max_parts) { return (1 + (size_t)max_b
 // LDS). Positions outside a sequence's block table give no entries and set
 // the position error bit.
 __global__ void __launch_bounds__(256) k_attn_plan(const int32_t* __restrict__ positions, int batch, int np2,
-                                                   int max_tokens, int32_t* __restrict__ plan,
+                                                   int max_tokens, int ptok, int32_t* __restrict__ plan,
                                                    uint32_t* __restrict__ err) {
   extern __shared__ int lds_plan[];
   int* s_key = lds_plan;     // [np2] tokens in the last partition (0: none)
@@ -61,8 +84,8 @@ __global__ void __launch_bounds__(256) k_attn_plan(const int32_t* __restrict__ p
     if (b < batch) {
       const int seq = positions[b] + 1;
       if (seq >= 1 && seq <= max_tokens) {
-        full = seq / kPartTokens;
-        rem = seq % kPartTokens;
+        full = seq / ptok;
+        rem = seq % ptok;
       } else {
         atomicOr(err, SIDP_DEVERR_POSITION);
       }
@@ -179,8 +202,12 @@ __device__ __forceinline__ void load_chunk(const AttnCall& a, const ChunkSrc& sr
   }
 }
 
+// Tokens from `te` on (the end of this wave's range) are masked; a chunk that
+// starts at or past `te` changes nothing: every score is -inf, so P is 0 and
+// alpha is 1 (or 0 while m_run is still -inf, when o and l_run are 0 anyway:
+// the exponents are then taken against 0 instead of -inf).
 template <int D>
-__device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t (&qb)[D / 32], int t0, int seq,
+__device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t (&qb)[D / 32], int t0, int te,
                                               int lane, float scale, float& m_run, float& l_run,
                                               f32x4_t (&o)[D / 16]) {
   constexpr int KK = D / 32, JD = D / 16;
@@ -193,28 +220,29 @@ __device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t 
     for (int kk = 0; kk < KK; kk++)
       s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(c.k[j][kk]), qb[kk], s[j], 0, 0, 0);
   }
-  const bool tail = t0 + 32 > seq;
+  const bool tail = t0 + 32 > te;
   float cmax = -INFINITY;
 #pragma unroll
   for (int j = 0; j < 2; j++)
 #pragma unroll
     for (int r = 0; r < 4; r++) {
       float v = s[j][r] * scale;
-      if (tail && t0 + 16 * j + lg * 4 + r >= seq) v = -INFINITY;
+      if (tail && t0 + 16 * j + lg * 4 + r >= te) v = -INFINITY;
       s[j][r] = v;
       cmax = fmaxf(cmax, v);
     }
   cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
   cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
   const float m_new = fmaxf(m_run, cmax);
-  const float alpha = exp2f(m_run - m_new);
+  const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = exp2f(m_run - m_ref);
   m_run = m_new;
   float p[8];
   float psum = 0.f;
 #pragma unroll
   for (int r = 0; r < 4; r++) {
-    p[r] = exp2f(s[0][r] - m_new);      // slots 0..3: block 0 tokens lg*4 + r
-    p[4 + r] = exp2f(s[1][r] - m_new);  // slots 4..7: block 1 tokens lg*4 + r
+    p[r] = exp2f(s[0][r] - m_ref);      // slots 0..3: block 0 tokens lg*4 + r
+    p[4 + r] = exp2f(s[1][r] - m_ref);  // slots 4..7: block 1 tokens lg*4 + r
     psum += p[r] + p[4 + r];
   }
   l_run = l_run * alpha + psum;
@@ -232,14 +260,14 @@ __device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t 
     u32x2_t v0 = c.v[jd][0], v1 = c.v[jd][1];
     if (tail) {  // invalid tokens may hold anything (NaN); zero them so 0 * V stays 0
       const int tb = t0 + lg * 4;
-      if (tb + 0 >= seq) v0.x &= 0xffff0000u;
-      if (tb + 1 >= seq) v0.x &= 0x0000ffffu;
-      if (tb + 2 >= seq) v0.y &= 0xffff0000u;
-      if (tb + 3 >= seq) v0.y &= 0x0000ffffu;
-      if (tb + 16 >= seq) v1.x &= 0xffff0000u;
-      if (tb + 17 >= seq) v1.x &= 0x0000ffffu;
-      if (tb + 18 >= seq) v1.y &= 0xffff0000u;
-      if (tb + 19 >= seq) v1.y &= 0x0000ffffu;
+      if (tb + 0 >= te) v0.x &= 0xffff0000u;
+      if (tb + 1 >= te) v0.x &= 0x0000ffffu;
+      if (tb + 2 >= te) v0.y &= 0xffff0000u;
+      if (tb + 3 >= te) v0.y &= 0x0000ffffu;
+      if (tb + 16 >= te) v1.x &= 0xffff0000u;
+      if (tb + 17 >= te) v1.x &= 0x0000ffffu;
+      if (tb + 18 >= te) v1.y &= 0xffff0000u;
+      if (tb + 19 >= te) v1.y &= 0x0000ffffu;
     }
     const bf16x8_t va = as_bf16x8(u32x4_t{v0.x, v0.y, v1.x, v1.y});
     o[jd] = o[jd] * alpha;
@@ -251,7 +279,7 @@ __device__ __forceinline__ void compute_chunk(const Chunk<D>& c, const bf16x8_t 
 __device__ __forceinline__ int seq_parts(const AttnCall& a, int b) {
   const int seq = a.positions[b] + 1;
   if (seq < 1 || seq > a.max_blocks * a.kv.bs) return 0;  // position outside its block table
-  return (seq + kPartTokens - 1) / kPartTokens;
+  return (seq + a.part_tokens - 1) / a.part_tokens;
 }
 
 // Item i of the work list is (entry i / Hkv of the plan, KV head i % Hkv).
@@ -286,14 +314,13 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     it.b = e & 0xffff;
     it.part = e >> 16;
     it.seq = positions[it.b] + 1;
-    it.nparts = (it.seq + kPartTokens - 1) / kPartTokens;
+    it.nparts = (it.seq + a.part_tokens - 1) / a.part_tokens;
     it.bt = (cint32_t*)(a.block_tables + (int64_t)it.b * a.max_blocks);
     // the partition's tokens split evenly over the four waves in whole 32-token
-    // chunks (kWaveTokens each for a full partition), so a sequence's shorter
-    // last partition keeps all four waves loading
-    const int len = min(it.seq - it.part * kPartTokens, kPartTokens);
+    // chunks, so a sequence's shorter last partition keeps all four waves loading
+    const int len = min(it.seq - it.part * a.part_tokens, a.part_tokens);
     const int share = ((len + 3) / 4 + 31) / 32 * 32;
-    it.tb = it.part * kPartTokens + wave * share;
+    it.tb = it.part * a.part_tokens + wave * share;
     it.te = min(it.tb + share, it.seq);
   };
   // the r-th item of this workgroup in snake order over the sorted list
@@ -332,8 +359,16 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     get_item(item, cur);
     bf16x8_t qb[KK];
     load_q(cur, qb);
+    // Wait for the first queries here, once: later the merge reuses dead
+    // query registers, and a load into them still pending on some path (a
+    // wave without tokens in its first item never reads qb) would make that
+    // reuse wait for every load in flight.
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++) asm volatile("" ::"v"(qb[kk]));
     Chunk<D> ca, cb;
-    if (cur.tb < cur.te) load_chunk<D>(a, ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb}, region_blk, k_lane, v_lane, bad, ca);
+    // (a wave without tokens in its first item reads the item's first chunk: masked)
+    load_chunk<D>(a, ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb < cur.te ? cur.tb : cur.part * a.part_tokens}, region_blk,
+                  k_lane, v_lane, bad, ca);
     for (;;) {
       const int nitem = item_of(round + 1);
       const bool has_next = nitem < total_items;
@@ -341,28 +376,37 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
       if (has_next) get_item(nitem, nx);
       const bool pf = has_next && nx.tb < nx.te;
       const int n = cur.te > cur.tb ? (cur.te - cur.tb + 31) / 32 : 0;  // this wave's chunks in the item
-      // source of stream slot i of this item (slot n is the prefetch)
+      // Chunks are taken in pairs, at least one pair per item: an odd count
+      // gets a masked extra chunk and a wave without tokens two, so that every
+      // path through an item issues its loads in the same order, the prefetch
+      // always lands in ca, and no wait the compiler places for a register
+      // reuse or copy reaches a load still in flight.
+      const int n2 = __builtin_amdgcn_readfirstlane(max(2, (n + 1) & ~1));
+      // source of stream slot i of this item (slot n2 is the prefetch; the
+      // extra chunk and a missing prefetch re-read the last chunk, or the
+      // item's first chunk when this wave has none: L2 hits)
       auto src_of = [&](int i) -> ChunkSrc {
         if (i < n) return ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb + 32 * i};
-        if (pf) return ChunkSrc{nx.bt, nx.seq, nx.g, nx.tb};
-        return ChunkSrc{cur.bt, cur.seq, cur.g, cur.tb + 32 * (n - 1)};
+        if (i == n2 && pf) return ChunkSrc{nx.bt, nx.seq, nx.g, nx.tb};
+        return ChunkSrc{cur.bt, cur.seq, cur.g, n > 0 ? cur.tb + 32 * (n - 1) : cur.part * a.part_tokens};
       };
 
       float m_run = -INFINITY, l_run = 0.f;
       f32x4_t o[JD];
 #pragma unroll
       for (int j = 0; j < JD; j++) o[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      for (int i = 0; i < n; i += 2) {
-        load_chunk<D>(a, src_of(i + 1), region_blk, k_lane, v_lane, bad, cb);
-        compute_chunk<D>(ca, qb, cur.tb + 32 * i, cur.seq, lane, scale, m_run, l_run, o);
-        if (i + 1 < n) {
-          load_chunk<D>(a, src_of(i + 2), region_blk, k_lane, v_lane, bad, ca);
-          compute_chunk<D>(cb, qb, cur.tb + 32 * (i + 1), cur.seq, lane, scale, m_run, l_run, o);
-        }
-      }
-      // an odd count left the prefetch in cb; an idle wave has not issued it yet
-      if (n == 0 && pf) load_chunk<D>(a, src_of(0), region_blk, k_lane, v_lane, bad, ca);
-      if (has_next) load_q(nx, qb);  // qb is dead until the next item's first chunk
+      int ci = 0;
+      do {
+        load_chunk<D>(a, src_of(ci + 1), region_blk, k_lane, v_lane, bad, cb);
+        compute_chunk<D>(ca, qb, cur.tb + 32 * ci, cur.te, lane, scale, m_run, l_run, o);
+        load_chunk<D>(a, src_of(ci + 2), region_blk, k_lane, v_lane, bad, ca);
+        compute_chunk<D>(cb, qb, cur.tb + 32 * (ci + 1), cur.te, lane, scale, m_run, l_run, o);
+        ci += 2;
+      } while (ci < n2);
+      // qb is dead until the next item's first chunk: load the next item's
+      // queries into it (this item's again when it is the last one, so that
+      // every path issues the same loads)
+      load_q(nx, qb);
 
       l_run += __shfl_xor(l_run, 16, 64);
       l_run += __shfl_xor(l_run, 32, 64);
@@ -375,34 +419,49 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
 #pragma unroll
         for (int r = 0; r < 4; r++) s_o[(wave * 16 + head) * (D + 1) + jd * 16 + lg * 4 + r] = o[jd][r];
       __syncthreads();
-      for (int i = threadIdx.x; i < group * D; i += 256) {
-        const int hh = i / D, d = i % D;
-        float M = -INFINITY;
+      // Merge the four waves' results: the output rows of a one-partition
+      // sequence, else the item's partial record (each wave writes whole
+      // lines of it, the first 32 threads its (m, l) line).
+      {
+        const int64_t row0 = (int64_t)cur.b * a.hq + cur.g * group;  // the group's first query head
+        const int rf = attn_rec_floats(group, D);
+        float* rec = a.part + ((int64_t)(cur.b * a.hkv + cur.g) * a.max_parts + cur.part) * rf;
+        for (int i = threadIdx.x; i < group * D; i += 256) {
+          const int hh = i / D, d = i % D;
+          float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
-        float L = 0.f, O = 0.f;
+          for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
+          float L = 0.f, O = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; w++) {
-          const float mw = s_m[w * 16 + hh];
-          const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-          L += s_l[w * 16 + hh] * f;
-          O += s_o[(w * 16 + hh) * (D + 1) + d] * f;
-        }
-        const int qh = cur.g * group + hh;
-        if (cur.nparts == 1) {
-          a.out[((int64_t)cur.b * a.hq + qh) * D + d] = f2bf(O / L);
-        } else {
-          float* pp = a.part + (((int64_t)cur.b * a.hq + qh) * a.max_parts + cur.part) * (D + 4);
-          pp[d] = O;
-          if (d == 0) {
-            pp[D] = M;
-            pp[D + 1] = L;
+          for (int w = 0; w < 4; w++) {
+            const float mw = s_m[w * 16 + hh];
+            const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+            L += s_l[w * 16 + hh] * f;
+            O += s_o[(w * 16 + hh) * (D + 1) + d] * f;
           }
+          if (cur.nparts == 1) a.out[(row0 + hh) * D + d] = f2bf(O / L);
+          else rec[i] = O;
+        }
+        if (cur.nparts > 1 && threadIdx.x < 32) {
+          const int t = threadIdx.x, hh = t >> 1;
+          float v = 0.f;
+          if (hh < group) {
+            float M = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w * 16 + hh]);
+            float L = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; w++) {
+              const float mw = s_m[w * 16 + hh];
+              L += s_l[w * 16 + hh] * ((mw == -INFINITY) ? 0.f : exp2f(mw - M));
+            }
+            v = (t & 1) ? L : M;
+          }
+          rec[group * D + t] = v;
         }
       }
       __syncthreads();  // s_m, s_l and s_o are reused by the next item
       if (!has_next) break;
-      if ((n & 1) && pf) ca = cb;
       cur = nx;
       item = nitem;
       round++;
@@ -417,25 +476,26 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
 // aligned). Partitions are summed in index order.
 template <int D>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnCall a) {
-  constexpr int RS = D + 4;
   const int g = blockIdx.x, b = blockIdx.y;
   const int group = a.hq / a.hkv;
   const int nparts = seq_parts(a, b);
   if (nparts <= 1) return;
+  const int rf = attn_rec_floats(group, D);
+  const float* recs = a.part + ((int64_t)b * a.hkv + g) * a.max_parts * rf;  // partition j at j * rf
   for (int i = threadIdx.x; i < group * (D / 4); i += 256) {
-    const int qh = g * group + i / (D / 4), d = (i % (D / 4)) * 4;
-    const float* p = a.part + ((int64_t)b * a.hq + qh) * a.max_parts * RS;
+    const int hh = i / (D / 4), d = (i % (D / 4)) * 4;
+    const float* ml = recs + group * D + 2 * hh;  // (m, l) of head hh, partition 0
     float M = -INFINITY;
-    for (int j = 0; j < nparts; j++) M = fmaxf(M, p[j * RS + D]);
+    for (int j = 0; j < nparts; j++) M = fmaxf(M, ml[j * rf]);
     float L = 0.f;
     f32x4_t O = {0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < nparts; j++) {
-      const float f = exp2f(p[j * RS + D] - M);
-      L += p[j * RS + D + 1] * f;
-      const f32x4_t v = *(const f32x4_t*)(p + j * RS + d);
+      const float f = exp2f(ml[j * rf] - M);
+      L += ml[j * rf + 1] * f;
+      const f32x4_t v = *(const f32x4_t*)(recs + j * rf + hh * D + d);
       O += v * f;
     }
-    uint16_t* o = a.out + ((int64_t)b * a.hq + qh) * D + d;
+    uint16_t* o = a.out + ((int64_t)b * a.hq + g * group + hh) * D + d;
     *(uint32_t*)o = pack_bf2(O[0] / L, O[1] / L);
     *(uint32_t*)(o + 2) = pack_bf2(O[2] / L, O[3] / L);
   }
@@ -447,7 +507,9 @@ hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s) {
   while (np2 < c.batch) np2 <<= 1;
   const size_t lds = (size_t)(2 * np2 + c.batch) * sizeof(int);
   if (lds > 64 * 1024) return hipErrorInvalidValue;
-  k_attn_plan<<<1, 256, lds, s>>>(c.positions, c.batch, np2, c.max_blocks * c.kv.bs, c.plan, c.err);
+  const int max_tokens = c.max_blocks * c.kv.bs;
+  const int ptok = attn_part_tokens_for(c.batch, c.hkv, max_tokens, c.num_cus);
+  k_attn_plan<<<1, 256, lds, s>>>(c.positions, c.batch, np2, max_tokens, ptok, c.plan, c.err);
   return hipGetLastError();
 }
 
@@ -463,9 +525,12 @@ static hipError_t launch_d(const AttnCall& c, int grid, int parts, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnCall& c, hipStream_t s) {
-  if (c.batch <= 0) return hipSuccess;
-  const int parts = (c.max_blocks * c.kv.bs + kPartTokens - 1) / kPartTokens;
+hipError_t launch_attention(const AttnCall& call, hipStream_t s) {
+  if (call.batch <= 0) return hipSuccess;
+  AttnCall c = call;
+  const int max_tokens = c.max_blocks * c.kv.bs;
+  c.part_tokens = attn_part_tokens_for(c.batch, c.hkv, max_tokens, c.num_cus);  // as the plan was built
+  const int parts = (max_tokens + c.part_tokens - 1) / c.part_tokens;
   if (parts > c.max_parts) return hipErrorInvalidValue;
   if (c.hq / c.hkv > 16) return hipErrorInvalidValue;
   const int grid = 2 * c.num_cus;  // persistent: two 4-wave workgroups per CU

@@ -293,7 +293,7 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   h->ws_bytes = ws;
   const int max_seq16 = round_up_i(c.max_seq_len, 16);
   h->attn_max_parts = (max_seq16 + attn_part_tokens() - 1) / attn_part_tokens();
-  const size_t part_bytes = attn_ws_bytes(c.max_batch, c.num_q_heads, c.head_dim, max_seq16);
+  const size_t part_bytes = attn_ws_bytes(c.max_batch, c.num_q_heads, c.num_kv_heads, c.head_dim, max_seq16);
   struct {
     void** p;
     size_t bytes;
@@ -677,6 +677,8 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
     a.positions = positions;
     a.batch = batch;
     a.max_blocks = max_blocks_per_seq;
+    a.hkv = c.num_kv_heads;
+    a.num_cus = h->num_cus;
     a.kv = kv_view(h);
     a.plan = h->attn_plan;
     a.err = h->err;
