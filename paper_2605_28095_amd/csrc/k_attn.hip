@@ -316,10 +316,12 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
     it.seq = positions[it.b] + 1;
     it.nparts = (it.seq + a.part_tokens - 1) / a.part_tokens;
     it.bt = (cint32_t*)(a.block_tables + (int64_t)it.b * a.max_blocks);
-    // the partition's tokens split evenly over the four waves in whole 32-token
-    // chunks, so a sequence's shorter last partition keeps all four waves loading
+    // the partition's tokens split evenly over the four waves in whole pairs of
+    // 32-token chunks (only the last wave's remainder can be an odd count, whose
+    // masked extra chunk re-reads HBM: non-temporal loads leave nothing in L2),
+    // so a sequence's shorter last partition keeps all four waves loading
     const int len = min(it.seq - it.part * a.part_tokens, a.part_tokens);
-    const int share = ((len + 3) / 4 + 31) / 32 * 32;
+    const int share = ((len + 3) / 4 + 63) / 64 * 64;
     it.tb = it.part * a.part_tokens + wave * share;
     it.te = min(it.tb + share, it.seq);
   };
@@ -377,7 +379,7 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
       const bool pf = has_next && nx.tb < nx.te;
       const int n = cur.te > cur.tb ? (cur.te - cur.tb + 31) / 32 : 0;  // this wave's chunks in the item
       // Chunks are taken in pairs, at least one pair per item: an odd count
-      // gets a masked extra chunk and a wave without tokens two, so that every
+      // gets a masked extra chunk, a wave without tokens two, so that every
       // path through an item issues its loads in the same order, the prefetch
       // always lands in ca, and no wait the compiler places for a register
       // reuse or copy reaches a load still in flight.
