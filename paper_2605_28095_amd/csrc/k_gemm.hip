@@ -109,7 +109,7 @@ struct GemmArgs {
   const uint16_t* w;   // packed
   int M, K, KP;        // KP = K rounded up to 64
   int NG;              // packed column groups (64 columns each)
-  int tiles;           // ceil(NG / kWaves)
+  int tiles;           // ceil(NG / waves per workgroup)
   int splits;
   int N;               // valid output columns (SWIGLU: F)
   int mblocks;         // row blocks of BM rows
@@ -132,11 +132,12 @@ __device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-// One workgroup: 4 waves. Wave wn computes rows [row0, row0 + MF*32) x the
-// 64 packed columns of group tile*4 + wn.
-template <int MF, int EPI, bool PARTIAL>
-__global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs a) {
-  constexpr int NT = 256;
+// One workgroup: W waves (4, or 8 for wide unsplit launches). Wave wn
+// computes rows [row0, row0 + MF*32) x the 64 packed columns of group
+// tile*W + wn; the activation tile staged in LDS serves all W waves.
+template <int MF, int EPI, bool PARTIAL, int W = kWaves>
+__global__ void __launch_bounds__(64 * W, 8 / W) k_gemm(GemmArgs a) {
+  constexpr int NT = 64 * W;
   constexpr int BM = MF * 32;
   constexpr int CPT = BM * 8 / NT;  // 16-byte X chunks per thread per stage (= MF)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -161,7 +162,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs a) {
   // wave index made provably uniform so weight offsets live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wn = wave;
-  const int ng = tile * kWaves + wn;
+  const int ng = tile * W + wn;
   const bool active = ng < a.NG;
   const int KT = a.KP / kBK;
   const int kt0 = (int)((int64_t)split * KT / a.splits);
@@ -416,26 +417,30 @@ hipError_t launch_pack_gate_up(const void* wg, const void* wu, int f, int k, voi
   return hipGetLastError();
 }
 
-template <int MF, int EPI, bool P>
+template <int MF, int EPI, bool P, int W = kWaves>
 static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
   constexpr int BM = MF * 32;
   a.mblocks = (a.M + BM - 1) / BM;
+  a.tiles = (a.NG + W - 1) / W;
   const size_t lds = (size_t)2 * BM * kBK * sizeof(uint16_t);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e =
-        hipFuncSetAttribute((const void*)k_gemm<MF, EPI, P>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipFuncSetAttribute((const void*)k_gemm<MF, EPI, P, W>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int pairs = a.tiles * a.splits;
   const int grid = (pairs + 7) / 8 * 8 * a.mblocks;
-  k_gemm<MF, EPI, P><<<grid, 256, lds, s>>>(a);
+  k_gemm<MF, EPI, P, W><<<grid, 64 * W, lds, s>>>(a);
   return hipGetLastError();
 }
 
 template <int EPI, bool P>
-static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+static hipError_t launch_epi(const GemmArgs& a, hipStream_t s, bool wide = false) {
+  if constexpr (!P) {
+    if (wide) return launch_mf<4, EPI, P, 8>(a, s);
+  }
   if (a.M <= 32) return launch_mf<1, EPI, P>(a, s);
   if (a.M <= 64) return launch_mf<2, EPI, P>(a, s);
   return launch_mf<4, EPI, P>(a, s);
@@ -461,11 +466,18 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
   const bool fuse_norm = c.norm_out && c.epilogue == SIDP_EPI_RESID && c.residual == c.out;
   if (c.norm_out && !fuse_norm) return hipErrorInvalidValue;
+  // Without a split, past 64 rows, an 8-wave workgroup (128 rows x 512
+  // columns) stages each activation tile once for twice the columns, so a
+  // wave issues 10 loads per k step instead of 12 (the projections pay per
+  // load instruction). It halves the workgroup count, so it is taken only
+  // while that still gives at least 0.8 workgroups per CU.
+  const bool wide = a.splits == 1 && c.m > 64 &&
+                    (int64_t)((a.NG + 7) / 8) * ((c.m + 127) / 128) * 10 >= (int64_t)8 * c.num_cus;
   hipError_t e;
   if (a.splits == 1) {
-    if (c.epilogue == SIDP_EPI_BF16) e = launch_epi<SIDP_EPI_BF16, false>(a, s);
-    else if (c.epilogue == SIDP_EPI_RESID) e = launch_epi<SIDP_EPI_RESID, false>(a, s);
-    else e = launch_epi<SIDP_EPI_SWIGLU, false>(a, s);
+    if (c.epilogue == SIDP_EPI_BF16) e = launch_epi<SIDP_EPI_BF16, false>(a, s, wide);
+    else if (c.epilogue == SIDP_EPI_RESID) e = launch_epi<SIDP_EPI_RESID, false>(a, s, wide);
+    else e = launch_epi<SIDP_EPI_SWIGLU, false>(a, s, wide);
     if (e != hipSuccess || !fuse_norm) return e;
     return launch_rmsnorm((const float*)c.out, c.norm_gain, c.norm_eps, c.norm_out, a.M, a.N, s);
   }

@@ -65,6 +65,7 @@ LINEAR_CASES = [
     (17, 4096, 2048, 1, False),
     (128, 3072, 1024, 1, False),   # three k-tiles per split: whole rounds of the three-deep ring only
     (100, 256, 45056, 0, True),    # enough column tiles for one split
+    (200, 512, 28672, 2, False),   # SwiGLU without a split past 64 rows: the gate/up launch of a decode step
 ]
 
 
