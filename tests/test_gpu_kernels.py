@@ -248,6 +248,25 @@ def test_attention_parity(lib, name, q_scale):
     assert_bf16_within_ulp(got, want, what="attention", abs_tol=2.0 ** -12 * pv)
 
 
+def _many_short_seqs(n=2048, seed=11):
+    return np.random.default_rng(seed).integers(1, 301, n).tolist()
+
+
+@pytest.mark.parametrize("hq,hkv,d,seqs", [
+    (16, 1, 128, ATTN_SEQS),   # the largest query group: 16 heads fill the MFMA columns and the (m, l) line
+    (8, 2, 64, ATTN_SEQS),     # head dim 64 over several partitions
+    (16, 1, 128, "many"),      # 2048 sequences x 1 KV head: whole-sequence items, no combine
+])
+def test_attention_parity_group_shapes(lib, hq, hkv, d, seqs):
+    cfg = synth.get_config("tiny_layer", num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
+    seqs = _many_short_seqs() if seqs == "many" else seqs
+    ctx, tables, nblk, k, v, q, maxb = _attn_setup(lib, cfg, seqs)
+    got = _attn_run(lib, cfg, ctx, tables, nblk, k, v, q, maxb)
+    want = _attn_oracle(cfg, ctx, tables, k, v, q)
+    pv = _attn_oracle(cfg, ctx, tables, k, v, q, absv=True)
+    assert_bf16_within_ulp(got, want, what=f"attention {hq}/{hkv} x {d}", abs_tol=2.0 ** -12 * pv)
+
+
 def test_attention_longest_context(lib):
     """A sequence at the longest context a handle accepts (2^20 positions:
     512 partitions merged by the combine kernel), ragged in its last block,
