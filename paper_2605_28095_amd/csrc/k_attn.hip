@@ -62,7 +62,7 @@ size_t attn_ws_bytes(int max_batch, int hq, int hkv, int d, int max_seq) {
 size_t attn_plan_bytes(int max_batch, int max_parts) { return (1 + (size_t)max_batch * max_parts) * sizeof(int32_t); }
 
 // The work list. plan[0] = number of (sequence, partition) entries; entry i is
-// plan[1 + i] = b | part << 16. Full 2048-token partitions come first, in
+// plan[1 + i] = b | part << 16. Full partitions (ptok tokens) come first, in
 // (b, part) order; then the last, shorter partition of every sequence that
 // has one, by decreasing length and then increasing b (a bitonic sort in
 // LDS). Positions outside a sequence's block table give no entries and set
@@ -473,9 +473,8 @@ __global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) 
 }
 
 // Log-sum-exp merge of a sequence's partitions: one workgroup per (KV head,
-// sequence) covering the group's query heads, four dims per thread (the
-// partial rows are padded to D + 4 floats so those loads are 16-byte
-// aligned). Partitions are summed in index order.
+// sequence) covering the group's query heads, four dims per thread (16-byte
+// loads from the partial records). Partitions are summed in index order.
 template <int D>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnCall a) {
   const int g = blockIdx.x, b = blockIdx.y;
