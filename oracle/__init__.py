@@ -55,4 +55,4 @@ from .decode import (  # noqa: F401
     decode_stack,
 )
 from .kvalloc import splitmix64_stream, fisher_yates, allocate_block_tables, slot_of  # noqa: F401
-from .schedule import was_schedule, owned, streamed_layer  # noqa: F401
+from .schedule import was_schedule, owned, streamed_layer, peak_shift_order  # noqa: F401

@@ -73,3 +73,25 @@ def streamed_layer(g, num_layers, ranks=0, rank=0):
     """The layer (0 .. L-1) that ring instance g computes."""
     streamed = [l for l in range(num_layers) if not owned(l, ranks, rank)]
     return streamed[g % len(streamed)]
+
+
+def peak_shift_order(num_layers, ranks, rank):
+    """§4.2 "Peak shifting": the order in which rank `rank` of `ranks` (d)
+    pulls the layers it does not own during one decode iteration. Layers form
+    cycles of d consecutive indices; in the cycle starting at layer c the rank
+    starts at layer c + rank and walks the cycle with wrap-around, skipping the
+    layer it owns (§4.1: layer l belongs to rank l mod d). Layers past the end
+    of the stack (a short last cycle) are left out. Returns a list of
+    (layer, owner) pairs, owner = layer mod d.
+
+    Reading: the text starts the walk at c + rank, which is the rank's own
+    layer when cycles start at multiples of d, so the first pull is c + rank + 1."""
+    d = ranks
+    order = []
+    for c in range(0, num_layers, d):
+        for k in range(d):
+            layer = c + (rank + k) % d
+            if layer >= num_layers or owned(layer, d, rank):
+                continue
+            order.append((layer, layer % d))
+    return order

@@ -501,3 +501,44 @@ def test_mode_schedule_invariants_on_random_traces():
                     assert all(b >= b_th * (1 + h) for b in window)
                 assert last is None or t - last >= W
                 last = t
+
+
+# ------------------------------------------------------------------ peak shifting (§4.2)
+
+def test_peak_shift_follows_the_text_on_one_cycle():
+    # d = 4, cycle starting at layer 0: rank 2 starts at layer 2 (its own, skipped) and
+    # wraps within the cycle: 3, 0, 1; rank 0 pulls 1, 2, 3; rank 3 pulls 0, 1, 2
+    assert [l for l, _ in oracle.peak_shift_order(4, 4, 2)] == [3, 0, 1]
+    assert [l for l, _ in oracle.peak_shift_order(4, 4, 0)] == [1, 2, 3]
+    assert [l for l, _ in oracle.peak_shift_order(4, 4, 3)] == [0, 1, 2]
+    assert oracle.peak_shift_order(7, 1, 0) == []  # one rank owns everything
+
+
+def test_peak_shift_covers_every_remote_layer_once():
+    # property (i): within each cycle a rank gets every layer it does not own after at
+    # most d - 1 pulls, never its own, and never one from outside the cycle
+    for d in range(2, 9):
+        for L in (d, 2 * d, 3 * d + 1, 5 * d - 1, 80):
+            for r in range(d):
+                order = oracle.peak_shift_order(L, d, r)
+                layers = [l for l, _ in order]
+                assert sorted(layers) == [l for l in range(L) if l % d != r], (d, L, r)
+                assert all(owner == l % d and owner != r for l, owner in order)
+                for c in range(0, L, d):
+                    in_cycle = [i for i, l in enumerate(layers) if c <= l < c + d]
+                    assert len(in_cycle) <= d - 1
+                    assert in_cycle == list(range(in_cycle[0], in_cycle[0] + len(in_cycle))) if in_cycle else True
+
+
+def test_peak_shift_spreads_each_step_over_distinct_owners():
+    # property (ii): at the k-th pull of a full cycle, the d ranks read d - 1 ... d
+    # different owners (the text says ranks "tend to" differ; this scheme makes it exact)
+    for d in range(2, 9):
+        L = 3 * d
+        orders = [oracle.peak_shift_order(L, d, r) for r in range(d)]
+        for cyc in range(L // d):
+            for k in range(d - 1):
+                owners = [orders[r][cyc * (d - 1) + k][1] for r in range(d)]
+                assert len(set(owners)) == d, (d, cyc, k, owners)
+                layers = [orders[r][cyc * (d - 1) + k][0] for r in range(d)]
+                assert all(cyc * d <= l < (cyc + 1) * d for l in layers)
