@@ -273,6 +273,21 @@ int sidp_cas_ffn(sidp_handle *h, int32_t layer, int32_t n_replicas, const void *
  * arguments are bad. */
 int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, int32_t *ops, int32_t *n_ops);
 
+/* ---- Peak-shifted pull order (host only; §4.2 "Peak shifting") ----
+ * With d = `ranks` ranks pooling their weights (layer l owned by rank l mod d,
+ * §4.1), the order in which rank `rank` pulls the layers it does not own
+ * during one decode iteration: layers form cycles of d consecutive indices,
+ * and in the cycle starting at layer c the rank walks c + rank, c + rank + 1,
+ * ... with wrap-around inside the cycle, skipping its own layer. So the k-th
+ * pulls of the d ranks in a full cycle all read different owners. Writes
+ * (layer, owner) pairs to `pairs` (host int32 [2 * *n], caller-owned; *n is
+ * the capacity in pairs on entry, the count on return, num_layers - ceil
+ * (num_layers / d) at most). This is the order a multi-GPU reader would issue
+ * its one-sided pulls in; on one GPU nothing is pulled. SIDP_EINVAL for
+ * num_layers < 1, ranks < 1, rank outside [0, ranks), a null n, a too-small
+ * capacity or a null pairs with a non-empty order. */
+int sidp_peak_shift_plan(int32_t num_layers, int32_t ranks, int32_t rank, int32_t *pairs, int32_t *n);
+
 /* ---- WaS / CaS mode choice (host only; §4.3 "Consistent mode switching") ----
  * The job orchestrator picks one mode for every engine of the group, so all
  * ranks agree on each layer's communication pattern. WaS stays while the

@@ -47,7 +47,7 @@ SIDP_POOL_FFN = 1
 EXPORTED = [
     "sidp_strerror", "sidp_last_hip_error", "sidp_create", "sidp_destroy", "sidp_layer_bytes",
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
-    "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
+    "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_peak_shift_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
     "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select", "sidp_mode_update",
 ]
@@ -113,6 +113,7 @@ _sigs = {
     "sidp_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _I, _P, _P]),
     "sidp_sync": (ctypes.c_int, [_P]),
     "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
+    "sidp_peak_shift_plan": (ctypes.c_int, [_I, _I, _I, _PI, _PI]),
     "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
     "sidp_cas_ffn": (ctypes.c_int, [_P, _I, _I, ctypes.POINTER(_P), _PI, ctypes.POINTER(_P), _P]),
     "sidp_timing_select": (ctypes.c_int, [_P, ctypes.c_uint32]),
@@ -239,6 +240,15 @@ def sidp_plan(num_layers, steps, ranks=0, rank=0):
     n = ctypes.c_int32(cap)
     _check(_lib.sidp_plan(num_layers, steps, ranks, rank, buf, ctypes.byref(n)), "sidp_plan")
     return [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n.value)]
+
+
+def sidp_peak_shift_plan(num_layers, ranks, rank):
+    """Peak-shifted pull order of one rank for one iteration, as (layer, owner)."""
+    cap = max(1, num_layers)
+    buf = (ctypes.c_int32 * (2 * cap))()
+    n = ctypes.c_int32(cap)
+    _check(_lib.sidp_peak_shift_plan(num_layers, ranks, rank, buf, ctypes.byref(n)), "sidp_peak_shift_plan")
+    return [(buf[2 * i], buf[2 * i + 1]) for i in range(n.value)]
 
 
 def sidp_mode_update(policy, state, active):

@@ -848,6 +848,24 @@ int sidp_timing_collect(sidp_handle* h, double* ms, int32_t* launches) {
   return SIDP_OK;
 }
 
+int sidp_peak_shift_plan(int32_t num_layers, int32_t ranks, int32_t rank, int32_t* pairs, int32_t* n) {
+  if (num_layers < 1 || ranks < 1 || rank < 0 || rank >= ranks || !n) return SIDP_EINVAL;
+  std::vector<int32_t> order;  // layers, in pull order
+  for (int64_t c = 0; c < num_layers; c += ranks)
+    for (int k = 1; k < ranks; k++) {  // k = 0 is the rank's own layer of the cycle
+      const int64_t layer = c + (rank + k) % ranks;
+      if (layer < num_layers) order.push_back((int32_t)layer);
+    }
+  if ((int64_t)order.size() > *n) return SIDP_EINVAL;
+  if (!order.empty() && !pairs) return SIDP_EINVAL;
+  for (size_t i = 0; i < order.size(); i++) {
+    pairs[2 * i] = order[i];
+    pairs[2 * i + 1] = order[i] % ranks;
+  }
+  *n = (int32_t)order.size();
+  return SIDP_OK;
+}
+
 int sidp_plan(int32_t num_layers, int32_t steps, int32_t ranks, int32_t rank, int32_t* ops_out, int32_t* n_ops) {
   if (num_layers < 1 || steps < 0 || !n_ops) return SIDP_EINVAL;
   if (ranks < 0 || (ranks > 0 && (rank < 0 || rank >= ranks))) return SIDP_EINVAL;

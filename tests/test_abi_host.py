@@ -167,3 +167,29 @@ def test_mode_update_rejects_bad_arguments():
         assert (st.mode, st.run) == (0, 0)  # unchanged
     with pytest.raises(sidp.SidpError):
         sidp.sidp_mode_update(sidp.sidp_mode_policy(8.0, 0.5, 3), st, [])
+
+
+def test_peak_shift_plan_matches_oracle():
+    import paper_2605_28095_amd as lib
+    for d in range(1, 9):
+        for L in (1, d, 2 * d + 1, 80):
+            for r in range(d):
+                assert lib.sidp_peak_shift_plan(L, d, r) == oracle.peak_shift_order(L, d, r), (L, d, r)
+
+
+def test_peak_shift_plan_rejects_bad_arguments():
+    import paper_2605_28095_amd as lib
+    n = ctypes.c_int32(100)
+    buf = (ctypes.c_int32 * 200)()
+    f = lib._lib.sidp_peak_shift_plan
+    E = lib.SIDP_EINVAL
+    assert f(0, 4, 0, buf, ctypes.byref(n)) == E
+    assert f(8, 0, 0, buf, ctypes.byref(n)) == E
+    assert f(8, 4, 4, buf, ctypes.byref(n)) == E
+    assert f(8, 4, -1, buf, ctypes.byref(n)) == E
+    assert f(8, 4, 0, buf, None) == E
+    small = ctypes.c_int32(5)  # rank 0 of 4 over 8 layers pulls 6
+    assert f(8, 4, 0, buf, ctypes.byref(small)) == E
+    assert f(8, 4, 0, None, ctypes.byref(n)) == E
+    one = ctypes.c_int32(0)
+    assert f(5, 1, 0, None, ctypes.byref(one)) == lib.SIDP_OK and one.value == 0  # nothing to pull
