@@ -136,10 +136,11 @@ __device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t
 // computes rows [row0, row0 + MF*32) x the 64 packed columns of group
 // tile*W + wn; the activation tile staged in LDS serves all W waves.
 template <int MF, int EPI, bool PARTIAL, int W = kWaves>
-__global__ void __launch_bounds__(64 * W, 8 / W) k_gemm(GemmArgs a) {
+__global__ void __launch_bounds__(64 * W, W > 4 ? 1 : 2) k_gemm(GemmArgs a) {
   constexpr int NT = 64 * W;
   constexpr int BM = MF * 32;
-  constexpr int CPT = BM * 8 / NT;  // 16-byte X chunks per thread per stage (= MF)
+  constexpr int CPT = (BM * 8 + NT - 1) / NT;  // 16-byte X chunks per thread per stage (the last may be idle)
+  constexpr bool kXTail = BM * 8 % NT != 0;     // 7-wave workgroups: not every thread has a last chunk
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   uint16_t* lds0 = smem;
   uint16_t* lds1 = smem + BM * kBK;
@@ -180,7 +181,7 @@ __global__ void __launch_bounds__(64 * W, 8 / W) k_gemm(GemmArgs a) {
 #pragma unroll
   for (int i = 0; i < CPT; i++) {
     const int ci = threadIdx.x + i * NT;
-    x_row[i] = ci >> 3;
+    x_row[i] = (!kXTail || ci < BM * 8) ? ci >> 3 : -1;  // -1: no chunk (out of range load, no store)
     x_cc[i] = ci & 7;
   }
 
@@ -204,7 +205,8 @@ __global__ void __launch_bounds__(64 * W, 8 / W) k_gemm(GemmArgs a) {
     for (int i = 0; i < CPT; i++) {
       const int row = row0 + x_row[i];
       const int k = kt * kBK + x_cc[i] * 8;
-      const uint32_t off = (row < a.M && k < a.K) ? (uint32_t)(((size_t)row * a.K + k) * 2) : kOutOfRange;
+      const bool in = (!kXTail || x_row[i] >= 0) && row < a.M && k < a.K;  // every thread issues the load
+      const uint32_t off = in ? (uint32_t)(((size_t)row * a.K + k) * 2) : kOutOfRange;
       xs[i] = buf_load16(xr_rsrc, off, 0);
     }
   };
@@ -212,6 +214,7 @@ __global__ void __launch_bounds__(64 * W, 8 / W) k_gemm(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < CPT; i++) {
       const int r = x_row[i];
+      if (kXTail && r < 0) continue;
       *(u32x4_t*)(lds + r * kBK + ((x_cc[i] ^ ((r >> 1) & 7)) << 3)) = xs[i];
     }
   };
@@ -440,9 +443,10 @@ static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
 }
 
 template <int EPI, bool P>
-static hipError_t launch_epi(const GemmArgs& a, hipStream_t s, bool wide = false) {
+static hipError_t launch_epi(const GemmArgs& a, hipStream_t s, int wide = 0) {
   if constexpr (!P) {
-    if (wide) return launch_mf<4, EPI, P, 8>(a, s);
+    if (wide == 7) return launch_mf<4, EPI, P, 7>(a, s);
+    if (wide == 8) return launch_mf<4, EPI, P, 8>(a, s);
   }
   if (a.M <= 32) return launch_mf<1, EPI, P>(a, s);
   if (a.M <= 64) return launch_mf<2, EPI, P>(a, s);
@@ -469,13 +473,24 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
   const bool fuse_norm = c.norm_out && c.epilogue == SIDP_EPI_RESID && c.residual == c.out;
   if (c.norm_out && !fuse_norm) return hipErrorInvalidValue;
-  // Without a split, past 64 rows, an 8-wave workgroup (128 rows x 512
-  // columns) stages each activation tile once for twice the columns, so a
-  // wave issues 10 loads per k step instead of 12 (the projections pay per
-  // load instruction). It halves the workgroup count, so it is taken only
-  // while that still gives at least 0.8 workgroups per CU.
-  const bool wide = a.splits == 1 && c.m > 64 &&
-                    (int64_t)((a.NG + 7) / 8) * ((c.m + 127) / 128) * 10 >= (int64_t)8 * c.num_cus;
+  // Without a split, past 64 rows, a 7- or 8-wave workgroup (128 rows x 448
+  // or 512 columns) stages each activation tile once for all its column
+  // groups, so a wave issues fewer loads per k step (the projections pay per
+  // load instruction). The width is chosen by the waves a CU runs to finish
+  // the grid: 4-wave workgroups go two to a CU (rounds of 8 waves), 7- and
+  // 8-wave ones one (rounds of 7 or 8), and a wide width is a candidate only
+  // while it gives at least 0.8 workgroups per CU (fewer would leave CUs idle
+  // that the model counts as busy); ties go to the wider one. A 70B-shaped
+  // gate/up (896 column groups) gets 7 waves at 256 rows, exactly 256
+  // workgroups; a 924-group one 8.
+  int wide = 0;
+  if (a.splits == 1 && c.m > 64) {
+    const int64_t mb = (c.m + 127) / 128, cus = std::max(1, c.num_cus);
+    const int64_t n4 = (a.NG + 3) / 4 * mb, n7 = (a.NG + 6) / 7 * mb, n8 = (a.NG + 7) / 8 * mb;
+    int64_t best = (n4 + 2 * cus - 1) / (2 * cus) * 8;
+    if (n7 * 10 >= 8 * cus && (n7 + cus - 1) / cus * 7 <= best) best = (n7 + cus - 1) / cus * 7, wide = 7;
+    if (n8 * 10 >= 8 * cus && (n8 + cus - 1) / cus * 8 <= best) best = (n8 + cus - 1) / cus * 8, wide = 8;
+  }
   hipError_t e;
   if (a.splits == 1) {
     if (c.epilogue == SIDP_EPI_BF16) e = launch_epi<SIDP_EPI_BF16, false>(a, s, wide);
