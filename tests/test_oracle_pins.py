@@ -435,6 +435,117 @@ def test_decode_layer_rows_independent():
         np.testing.assert_array_equal(one[0], full[b])
 
 
+def _bf(t):
+    """torch float64 -> nearest bfloat16 (round to nearest even through float32,
+    torch's own conversion), back as float64."""
+    return t.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+def _attention_block_by_torch(x, lw, cfg, kc, vc, pos, tabs):
+    """The attention sub-block of one decode step with bf16 storage at the
+    model's storage points (normed input, projection outputs, rotated q and k,
+    cached v, attention output), built from torch library routines in float64
+    (rms_norm, matmul, complex-multiplication RoPE, scaled_dot_product_attention)
+    and torch's bf16 conversion. Returns the new tokens' cached k and v
+    (B, Hkv, D) and the attention output o (B, Hq * D)."""
+    H, Hq, Hkv, D, bs = cfg["hidden"], cfg["num_q_heads"], cfg["num_kv_heads"], cfg["head_dim"], cfg["block_size"]
+    w = {n: torch.from_numpy(od.bf16_bits_to_f64(a)) for n, a in lw.items()}
+    xt = torch.from_numpy(x)
+    B = xt.shape[0]
+    h = _bf(F.rms_norm(xt, (H,), weight=w["g_attn"], eps=cfg["rms_eps"]))
+    q = _bf(h @ w["w_q"].T).reshape(B, Hq, D)
+    k = _bf(h @ w["w_k"].T).reshape(B, Hkv, D)
+    v = _bf(h @ w["w_v"].T).reshape(B, Hkv, D)
+    p = np.asarray(pos)[:, None, None]
+    q = _bf(torch.from_numpy(_rope_complex(q.numpy(), p, cfg["rope_theta"])))
+    k = _bf(torch.from_numpy(_rope_complex(k.numpy(), p, cfg["rope_theta"])))
+    o = torch.empty(B, Hq, D, dtype=torch.float64)
+    for b in range(B):
+        c = int(pos[b])
+        K = torch.cat([torch.from_numpy(_gather(kc, tabs[b], c, bs)), k[b][None]], 0).permute(1, 0, 2)  # (Hkv, c+1, D)
+        V = torch.cat([torch.from_numpy(_gather(vc, tabs[b], c, bs)), v[b][None]], 0).permute(1, 0, 2)
+        rep = Hq // Hkv
+        o[b] = F.scaled_dot_product_attention(q[b][:, None], K.repeat_interleave(rep, 0).contiguous(),
+                                              V.repeat_interleave(rep, 0).contiguous())[:, 0]
+    return k.numpy(), v.numpy(), _bf(o.reshape(B, Hq * D)).numpy()
+
+
+def _is_bf16(a):
+    return np.array_equal(od.round_to_bf16(a), a)
+
+
+def _pass_through_attention(lw, cfg):
+    """W_o = identity (the attention output lands unchanged on the residual),
+    W_down = 0 (the FFN adds nothing): x2 - x is the stored attention output."""
+    lz = dict(lw)
+    one = np.uint16(0x3F80)  # bf16 1.0
+    lz["w_o"] = (np.eye(cfg["hidden"], cfg["num_q_heads"] * cfg["head_dim"]) * one).astype(np.uint16)
+    lz["w_down"] = np.zeros_like(lw["w_down"])
+    return lz
+
+
+def test_attention_storage_points_exact_case():
+    """Every token attends only to itself (empty contexts), so o equals the new v
+    exactly; each v element sums two normed inputs with weight 1.0, so the
+    float64 arithmetic is exact and the only roundings are the storage points.
+    Rounding the normed input h first, then the sum, differs from rounding the
+    sum once: the pin fails if h is not stored in bf16. The cached v must be
+    bf16 (fails if the projection output is not rounded)."""
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    H, KD = cfg["hidden"], cfg["num_kv_heads"] * cfg["head_dim"]
+    wv = np.zeros((KD, H), np.uint16)
+    j = np.arange(KD)
+    wv[j, 2 * j] = wv[j, 2 * j + 1] = 0x3F80
+    lz = _pass_through_attention(dict(lw, w_v=wv), cfg)
+    pos = np.zeros(cfg["batch"], np.int64)
+    tabs0 = np.array(ka.allocate_block_tables(pos, 1, cfg["num_phys_blocks"], 5, 0))
+    kc1, vc1 = kc.copy(), vc.copy()
+    out = od.decode_layer(x, lz, cfg, kc1, vc1, pos, tabs0, round_bf16=True)
+    k_t, v_t, o_t = _attention_block_by_torch(x, lz, cfg, kc, vc, pos, tabs0)
+    np.testing.assert_array_equal(out - x, o_t)
+    for b in range(cfg["batch"]):
+        blk = tabs0[b][0]
+        np.testing.assert_array_equal(vc1[blk, :, 0, :], v_t[b])
+        np.testing.assert_array_equal(kc1[blk, :, 0, :], k_t[b])
+    # the case does tell the two orders of rounding apart
+    h = F.rms_norm(torch.from_numpy(x), (H,), weight=torch.from_numpy(od.bf16_bits_to_f64(lw["g_attn"])),
+                   eps=cfg["rms_eps"])
+    once = _bf(h @ torch.from_numpy(od.bf16_bits_to_f64(wv)).T).numpy()
+    assert np.mean(once != v_t.reshape(cfg["batch"], KD)) > 0.05
+
+
+def test_attention_storage_points_cached_contexts():
+    """Random weights, contexts 16..64: the new key and value written to the
+    cache are bf16 numbers (fails if the rotated k or the projected v is left
+    unrounded) and match the torch evaluation; the attention output matches it
+    too (fails if the rotated q or the normed input is left unrounded: the
+    scores move, and the output rounds differently in many places). Float64
+    summation order may flip a rounding at a boundary, so a handful of
+    elements may differ by one bf16 step; a missing storage rounding moves
+    far more."""
+    cfg = synth.get_config("tiny_layer")
+    w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
+    lz = _pass_through_attention(lw, cfg)
+    kc1, vc1 = kc.copy(), vc.copy()
+    out = od.decode_layer(x, lz, cfg, kc1, vc1, ctx, tabs, round_bf16=True)
+    k_t, v_t, o_t = _attention_block_by_torch(x, lz, cfg, kc, vc, ctx, tabs)
+    bs = cfg["block_size"]
+    kn = np.stack([kc1[tabs[b][c // bs], :, c % bs, :] for b, c in enumerate(ctx)])
+    vn = np.stack([vc1[tabs[b][c // bs], :, c % bs, :] for b, c in enumerate(ctx)])
+    got_o = out - x
+
+    def close(got, want, what):
+        assert _is_bf16(got), f"{what}: not bf16 numbers"
+        d = got != want
+        assert d.mean() <= 0.01, f"{what}: {d.mean():.2%} of elements differ"
+        np.testing.assert_allclose(got, want, rtol=2.0 ** -7, atol=0)
+
+    close(kn, k_t, "cached k")
+    close(vn, v_t, "cached v")
+    close(got_o, o_t, "attention output")
+
+
 def test_bf16_mode_close_to_exact_mode():
     cfg = synth.get_config("tiny_layer")
     w, lw, ctx, tabs, kc, vc, x = _tiny_inputs(cfg)
