@@ -146,7 +146,9 @@ int sidp_pool_init(sidp_handle *h, void *pool, size_t pool_bytes, void *slots, s
 /* Packs one layer's weights (device pointers, layout above) into its pool
  * blob: norm gains, QKV bias, then the QKV, O, interleaved gate/up and down
  * matrices re-laid into the GEMM's fragment order. Asynchronous on `stream`;
- * the sources may be freed once the stream has passed this call. */
+ * the sources may be freed once the stream has passed this call. Restarts
+ * the slot ring (the slots may hold the layer's old blob): call it only when
+ * no decode step is in flight on the handle, i.e. after sidp_sync. */
 int sidp_pool_load_layer(sidp_handle *h, int32_t layer, const sidp_layer_weights *w, void *stream);
 
 /* ---- paged KV cache (per-request KV state, §2.2) ----
@@ -189,7 +191,11 @@ int sidp_kv_attach(sidp_handle *h, void *k_cache, void *v_cache, int32_t num_phy
  * for layer g's compute to release the slot. The copy stream thus runs two
  * layers ahead, into the next call's first layers too. RESIDENT and STREAMED
  * give bit-identical results (the paper's modes change only where weights
- * live, §4.1). Returns without waiting for the GPU. */
+ * live, §4.1). Returns without waiting for the GPU.
+ * Calls that use the handle's own buffers (decode steps, sidp_cas_ffn,
+ * sidp_linear, sidp_attention) are ordered as if on one stream: a call on a
+ * compute stream other than the previous call's first waits (on the device)
+ * for the previous call's work to finish. */
 int sidp_decode_step(sidp_handle *h, float *hidden, const int32_t *positions, const int32_t *block_tables,
                      int32_t max_blocks_per_seq, int32_t batch, int32_t flags, void *compute, void *copy);
 /* Waits for all work the handle enqueued on both streams; returns
@@ -226,6 +232,19 @@ int sidp_timing_select(sidp_handle *h, uint32_t class_mask);
 #define SIDP_POOL_LAYER 0
 #define SIDP_POOL_FFN   1
 int sidp_set_pooling(sidp_handle *h, int32_t mode, int32_t ranks, int32_t rank);
+
+/* ---- fill tiles (§4.2 "Asynchronous one-sided reading": a layer is fetched
+ * in tensor tiles, each with its own completion notification) ----
+ * A streamed layer's fill is two tiles on the copy stream: the first
+ * `first_tile_percent` percent of the staged bytes as soon as the slot is
+ * released, the rest once the previous layer's attention half has been
+ * issued, so that it runs beside that layer's projections. loads_a and
+ * loads_b are the 16-byte loads each lane of the fill kernel keeps in flight
+ * in the two tiles (2, 4 or 8; 0 = the default for the step's batch: 4 and 2
+ * from 128 rows up, 8 and 4 below). Defaults: 25, 0, 0. Takes effect from the
+ * next decode step. SIDP_EINVAL for a percent outside [0, 100] or another
+ * load count. */
+int sidp_set_fill_tiles(sidp_handle *h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b);
 
 /* ---- Compute-as-a-Service, owner side ----
  * §4.3: in the small-batch tail, non-owner replicas send their FFN inputs to
@@ -316,6 +335,15 @@ typedef struct {
 } sidp_mode_state;
 int sidp_mode_update(const sidp_mode_policy *policy, sidp_mode_state *state, int32_t n_engines, const int32_t *active,
                      int32_t *mode);
+
+/* ---- failure injection (tests of the error contract) ----
+ * Makes the next HIP runtime call that the handle checks fail with
+ * `hip_error` (a non-zero hipError_t value) before reaching the runtime, as
+ * if the runtime had returned it: that call returns SIDP_EHIP,
+ * sidp_last_hip_error reports hip_error, and the handle is poisoned (later
+ * calls return SIDP_ESTATE; sidp_destroy still frees it). No GPU work is
+ * faulted. SIDP_EINVAL for hip_error 0. */
+int sidp_debug_inject_hip_error(sidp_handle *h, int32_t hip_error);
 
 /* ---- single kernels, for parity checks and reuse ----
  * All enqueue on `stream` and return immediately. */

@@ -50,6 +50,7 @@ EXPORTED = [
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_peak_shift_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
     "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select", "sidp_mode_update",
+    "sidp_set_fill_tiles", "sidp_debug_inject_hip_error",
 ]
 
 SIDP_CAS_MAX_REPLICAS = 16
@@ -115,6 +116,8 @@ _sigs = {
     "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
     "sidp_peak_shift_plan": (ctypes.c_int, [_I, _I, _I, _PI, _PI]),
     "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
+    "sidp_set_fill_tiles": (ctypes.c_int, [_P, _I, _I, _I]),
+    "sidp_debug_inject_hip_error": (ctypes.c_int, [_P, _I]),
     "sidp_cas_ffn": (ctypes.c_int, [_P, _I, _I, ctypes.POINTER(_P), _PI, ctypes.POINTER(_P), _P]),
     "sidp_timing_select": (ctypes.c_int, [_P, ctypes.c_uint32]),
     "sidp_rmsnorm": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I, _I, _P]),
@@ -275,6 +278,14 @@ def mode_schedule(b_th, hysteresis, window, batches):
 
 def sidp_set_pooling(h, mode, ranks=0, rank=0):
     _check(_lib.sidp_set_pooling(h, mode, ranks, rank), "sidp_set_pooling")
+
+
+def sidp_set_fill_tiles(h, first_tile_percent=25, loads_a=0, loads_b=0):
+    _check(_lib.sidp_set_fill_tiles(h, first_tile_percent, loads_a, loads_b), "sidp_set_fill_tiles")
+
+
+def sidp_debug_inject_hip_error(h, hip_error):
+    _check(_lib.sidp_debug_inject_hip_error(h, hip_error), "sidp_debug_inject_hip_error")
 
 
 def sidp_cas_ffn(h, layer, xs, rows, ys, stream=None):

@@ -5,8 +5,6 @@
 // copy on the CUs; a copy kernel of our own lets the runtime choose how many
 // workgroups (CUs) the fill may occupy while compute runs beside it.
 // Also: a NaN poison fill and a bounded spin, used to expose missing waits.
-#include <cstdlib>
-
 #include "common.h"
 #include "internal.h"
 
@@ -99,14 +97,26 @@ static hipError_t launch_fill_u(const void* src, void* dst, size_t bytes, int nu
   return hipGetLastError();
 }
 
+// The kernel addresses a launch's range with 32-bit buffer offsets, so a
+// range past 1 GiB is filled by several launches of at most 1 GiB each, back
+// to back on the stream (same engine, same grid).
+constexpr size_t kFillChunk = (size_t)1 << 30;
+
 hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, int loads, hipStream_t s) {
-  if (bytes == 0) return hipSuccess;
-  if (bytes % 16 || bytes >= ((size_t)1 << 31)) return launch_copy(src, dst, bytes, 0, s);
-  switch (loads) {
-    case 8: return launch_fill_u<8>(src, dst, bytes, num_cus, s);
-    case 4: return launch_fill_u<4>(src, dst, bytes, num_cus, s);
-    default: return launch_fill_u<2>(src, dst, bytes, num_cus, s);
+  if (bytes % 16) return hipErrorInvalidValue;  // slot ranges are 256-byte aligned
+  for (size_t off = 0; off < bytes; off += kFillChunk) {
+    const size_t n = bytes - off < kFillChunk ? bytes - off : kFillChunk;
+    const uint8_t* sp = (const uint8_t*)src + off;
+    uint8_t* dp = (uint8_t*)dst + off;
+    hipError_t e;
+    switch (loads) {
+      case 8: e = launch_fill_u<8>(sp, dp, n, num_cus, s); break;
+      case 4: e = launch_fill_u<4>(sp, dp, n, num_cus, s); break;
+      default: e = launch_fill_u<2>(sp, dp, n, num_cus, s); break;
+    }
+    if (e != hipSuccess) return e;
   }
+  return hipSuccess;
 }
 
 __global__ void k_copy_tail(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, size_t n) {

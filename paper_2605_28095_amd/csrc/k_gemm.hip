@@ -27,8 +27,6 @@
 //    or by the kernel that consumes the result (the RoPE/KV-append kernel for
 //    QKV, the residual + RMSNorm reduction for O and down; LinearCall's
 //    defer_reduce and norm_out select this).
-#include <cstdlib>
-
 #include "common.h"
 #include "internal.h"
 
@@ -376,14 +374,7 @@ int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   // hiding gains. Rounding down rather than to nearest keeps a few CUs from
   // running a second workgroup after the rest have finished (O and down at
   // M=384: 192 workgroups instead of 288, the step 2% faster).
-  // SIDP_SPLIT_TARGET overrides the target, in percent of the CU count.
-  static int pct = -1;
-  if (pct < 0) {
-    const char* e = std::getenv("SIDP_SPLIT_TARGET");
-    pct = e ? std::max(10, std::atoi(e)) : 100;
-  }
-  const int target = pct * num_cus / 100;
-  int s = target / base;
+  int s = num_cus / base;
   if (s < 1) s = 1;
   if (s > 16) s = 16;
   if (s > KT) s = KT;

@@ -32,6 +32,7 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
 constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
 constexpr int kFillSmallBatch = 128;   // below this many rows the fill runs with more loads in flight
+constexpr int kBurstGrid = 512;        // workgroups of the whole-chip burst copy (SIDP_COPY_BURST)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up_i(int a, int b) { return (a + b - 1) / b * b; }
@@ -153,6 +154,9 @@ void build_step(int L, int ranks, int rank, int64_t step, int64_t* ring_g, bool*
 
 }  // namespace
 
+struct sidp_handle;
+static hipError_t take_injected(sidp_handle* h);
+
 struct sidp_handle {
   sidp_config cfg;
   BlobLayout blob;
@@ -184,6 +188,11 @@ struct sidp_handle {
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
+  // Recorded on the compute stream after each call that uses the handle's
+  // buffers; a later call on another stream waits for it first.
+  hipEvent_t work_done = nullptr;
+  bool work_recorded = false;
+  int inject_hip = 0;  // sidp_debug_inject_hip_error: the next checked HIP call fails with this code
   int fill_pct = 0;       // percent of the staged range in fill part A
   // 16-byte loads in flight per lane of the background fill. Part A starts when
   // the slot is released and mostly overlaps the next layer's QKV projection and
@@ -200,7 +209,6 @@ struct sidp_handle {
   // ring state
   bool ring_started = false;
   int64_t ring_g = 0;  // global index of the next streamed layer
-  int copy_grid = 512;
   hipStream_t last_compute = nullptr, last_copy = nullptr;
   bool any_copy = false;
   // SIDP_TIMING: event pairs per kernel class launch, recycled by sidp_timing_collect
@@ -214,10 +222,16 @@ struct sidp_handle {
   uint32_t timing_mask = (1u << SIDP_NUM_KCLASSES) - 1;  // classes SIDP_TIMING brackets
 };
 
-#define HIPCHK(h, expr)                \
-  do {                                 \
-    hipError_t e_ = (expr);            \
-    if (e_ != hipSuccess) {            \
+static hipError_t take_injected(sidp_handle* h) {
+  const hipError_t e = (hipError_t)h->inject_hip;
+  h->inject_hip = 0;
+  return e;
+}
+
+#define HIPCHK(h, expr)                                                      \
+  do {                                                                       \
+    hipError_t e_ = (h)->inject_hip ? take_injected(h) : (hipError_t)(expr); \
+    if (e_ != hipSuccess) {                                                  \
       (h)->last_hip = (int)e_;         \
       (h)->poisoned = true;            \
       return SIDP_EHIP;                \
@@ -254,6 +268,7 @@ static void free_device(sidp_handle* h) {
     if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
     if (h->mid[i]) (void)hipEventDestroy(h->mid[i]);
   }
+  if (h->work_done) (void)hipEventDestroy(h->work_done);
   for (auto& t : h->timed) {
     (void)hipEventDestroy(t.a);
     (void)hipEventDestroy(t.b);
@@ -279,7 +294,6 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   if (hipGetDevice(&h->device) != hipSuccess) return fail(SIDP_EHIP);
   if (hipDeviceGetAttribute(&h->num_cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess)
     return fail(SIDP_EHIP);
-  if (const char* g = std::getenv("SIDP_COPY_GRID")) h->copy_grid = std::max(1, std::atoi(g));
 
   const size_t B = (size_t)c.max_batch, H = (size_t)c.hidden, D = (size_t)c.head_dim;
   const size_t QD = (size_t)c.num_q_heads * D;
@@ -331,10 +345,8 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
     if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->mid[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
   }
+  if (hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
   h->fill_pct = kFillPartAPercent;
-  if (const char* e = std::getenv("SIDP_FILL_SPLIT")) h->fill_pct = std::min(100, std::max(0, std::atoi(e)));
-  if (const char* e = std::getenv("SIDP_FILL_LOADS_A")) h->fill_loads_a = std::atoi(e);
-  if (const char* e = std::getenv("SIDP_FILL_LOADS_B")) h->fill_loads_b = std::atoi(e);
   for (int l = 0; l < c.num_layers; l++) h->streamed_layers.push_back(l);
   *out = h;
   return SIDP_OK;
@@ -396,6 +408,9 @@ int sidp_pool_load_layer(sidp_handle* h, int32_t layer, const sidp_layer_weights
   HIPCHK(h, launch_pack_gate_up(w->w_gate, w->w_up, c.ffn_dim, (int)H, base + h->blob.w_gu, s));
   HIPCHK(h, launch_pack_linear(w->w_down, (int)H, c.ffn_dim, base + h->blob.w_d, s));
   h->loaded[layer] = 1;
+  // the slots may hold (or be filling) the layer's old blob: restart the ring
+  h->ring_started = false;
+  h->ring_g = 0;
   return SIDP_OK;
 }
 
@@ -460,6 +475,19 @@ static KvView kv_view(const sidp_handle* h) {
   v.d = h->cfg.head_dim;
   v.bs = h->cfg.block_size;
   return v;
+}
+
+// Calls that use the handle's buffers (activations, partials, work list) are
+// ordered like one stream: a call on a stream other than the previous call's
+// first waits for the previous call's work (the event recorded after it).
+static hipError_t begin_call(sidp_handle* h, hipStream_t s) {
+  if (h->work_recorded && s != h->last_compute) return hipStreamWaitEvent(s, h->work_done, 0);
+  return hipSuccess;
+}
+static hipError_t finish_call(sidp_handle* h, hipStream_t s) {
+  h->last_compute = s;
+  h->work_recorded = true;
+  return hipEventRecord(h->work_done, s);
 }
 
 static LinearCall linear_call(const sidp_handle* h, const void* x, int m, int k, const void* packed, int n, int epi,
@@ -642,7 +670,7 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
   else if (flags & SIDP_COPY_SDMA) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDeviceNoCU, cp);
-  else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, h->copy_grid, cp);
+  else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, kBurstGrid, cp);
   else {
     const bool small = h->step_batch < kFillSmallBatch;
     const int la = h->fill_loads_a ? h->fill_loads_a : (small ? 8 : 4);
@@ -670,7 +698,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   h->step_batch = batch;
   hipStream_t cs = (hipStream_t)compute, cp = (hipStream_t)copy;
   if (streamed && (!h->slots || cp == cs)) return SIDP_EINVAL;
-  h->last_compute = cs;
+  HIPCHK(h, begin_call(h, cs));
   {
     // the attention work list depends on the positions only: one per step
     AttnCall a{};
@@ -689,6 +717,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
     for (int l = 0; l < c.num_layers; l++)
       HIPCHK(h, run_layer(h, h->pool + (size_t)l * h->blob.total, l, hidden, positions, block_tables,
                           max_blocks_per_seq, batch, cs));
+    HIPCHK(h, finish_call(h, cs));
     return SIDP_OK;
   }
 
@@ -742,6 +771,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         break;
     }
   }
+  HIPCHK(h, finish_call(h, cs));
   return SIDP_OK;
 }
 
@@ -786,13 +816,14 @@ int sidp_cas_ffn(sidp_handle* h, int32_t layer, int32_t n_replicas, const void* 
   out.gather = 0;
   hipStream_t s = (hipStream_t)stream;
   const uint8_t* wb = h->pool + (size_t)layer * h->blob.total;
+  HIPCHK(h, begin_call(h, s));
   HIPCHK(h, launch_rows_move(in, s));
   HIPCHK(h, launch_linear(linear_call(h, h->h, total, H, wb + h->blob.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr,
                                       nullptr, h->act), s));
   HIPCHK(h, launch_linear(linear_call(h, h->act, total, c.ffn_dim, wb + h->blob.w_d, H, SIDP_EPI_RESID, nullptr,
                                       nullptr, h->cas_y), s));
   HIPCHK(h, launch_rows_move(out, s));
-  h->last_compute = s;
+  HIPCHK(h, finish_call(h, s));
   return SIDP_OK;
 }
 
@@ -810,6 +841,25 @@ int sidp_set_pooling(sidp_handle* h, int32_t mode, int32_t ranks, int32_t rank) 
   // the slots no longer hold what the ring expects: restart it
   h->ring_started = false;
   h->ring_g = 0;
+  return SIDP_OK;
+}
+
+int sidp_set_fill_tiles(sidp_handle* h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b) {
+  if (!h) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  auto loads_ok = [](int32_t n) { return n == 0 || n == 2 || n == 4 || n == 8; };
+  if (first_tile_percent < 0 || first_tile_percent > 100 || !loads_ok(loads_a) || !loads_ok(loads_b))
+    return SIDP_EINVAL;
+  h->fill_pct = first_tile_percent;
+  h->fill_loads_a = loads_a;
+  h->fill_loads_b = loads_b;
+  return SIDP_OK;
+}
+
+int sidp_debug_inject_hip_error(sidp_handle* h, int32_t hip_error) {
+  if (!h || hip_error == 0) return SIDP_EINVAL;
+  if (h->poisoned) return SIDP_ESTATE;
+  h->inject_hip = hip_error;
   return SIDP_OK;
 }
 
@@ -940,8 +990,9 @@ int sidp_linear(sidp_handle* h, const void* x, int32_t m, int32_t k, const void*
   const int ncols = epilogue == SIDP_EPI_SWIGLU ? 2 * round_up_i(n, 32) : n;
   if (!gemm_fits(m, ncols, k)) return SIDP_EINVAL;
   if (gemm_ws_bytes(m, ncols, k, h->num_cus) > h->ws_bytes) return SIDP_EINVAL;
+  HIPCHK(h, begin_call(h, (hipStream_t)stream));
   HIPCHK(h, launch_linear(linear_call(h, x, m, k, packed, n, epilogue, bias, residual, out), (hipStream_t)stream));
-  h->last_compute = (hipStream_t)stream;
+  HIPCHK(h, finish_call(h, (hipStream_t)stream));
   return SIDP_OK;
 }
 
@@ -1015,9 +1066,10 @@ int sidp_attention(sidp_handle* h, const void* q, int32_t region, const int32_t*
   a.err = h->err;
   a.num_cus = h->num_cus;
   a.plan = h->attn_plan;
+  HIPCHK(h, begin_call(h, (hipStream_t)stream));
   HIPCHK(h, launch_attn_plan(a, (hipStream_t)stream));
   HIPCHK(h, launch_attention(a, (hipStream_t)stream));
-  h->last_compute = (hipStream_t)stream;
+  HIPCHK(h, finish_call(h, (hipStream_t)stream));
   return SIDP_OK;
 }
 

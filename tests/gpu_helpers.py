@@ -157,5 +157,20 @@ class Stack:
             x = oracle.decode_stack(x, self.layer_weights, self.cfg, kr, vr, pos + s, tabs, round_bf16)
         return x, kr, vr, tabs
 
+    def run_oracle_both(self, rows):
+        """One step of the whole stack for `rows` in both oracle evaluations
+        (bf16 storage rounding, exact), fetching each layer's weights once."""
+        x, kr, vr, pos, tabs = self.oracle_inputs(rows)
+        kr2, vr2 = [k.copy() for k in kr], [v.copy() for v in vr]
+        xb, xe = x, x.copy()
+        R = len(kr)
+        for l in range(self.cfg["num_layers"]):
+            w = self.layer_weights(l)
+            xb = oracle.decode_layer(xb, w, self.cfg, kr[l % R], vr[l % R], pos, tabs, True)
+            xe = oracle.decode_layer(xe, w, self.cfg, kr2[l % R], vr2[l % R], pos, tabs, False)
+            if (l + 1) % 10 == 0:
+                print(f"oracle: {l + 1} of {self.cfg['num_layers']} layers", flush=True)
+        return xb, xe
+
     def close(self):
         self.dec.close()

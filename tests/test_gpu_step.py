@@ -12,9 +12,11 @@ near a rounding boundary) perturbs the next layers' inputs and flips further
 roundings, so two valid bf16 evaluations drift apart about as far as the
 bf16-rounding oracle drifts from the exact one (about 1e-2 after 8
 layers of the 72B shape). On the 80-layer 70B-shaped stack that drift of the
-oracle's own two evaluations reaches 2.8-3.3e-2 per row (measured), past the
-2e-2 bar: there the full-depth check uses 2x that drift, 6.5e-2, and the 2e-2
-bar is checked on the first 10 layers of the same full-size configuration.
+oracle's own two evaluations is about 3e-2 per row, past the 2e-2 bar: there
+the full-depth check computes both oracle evaluations for three rows in the
+same run and holds the GPU's error against the exact oracle to max(2e-2, 2x
+that row's drift); the 2e-2 bar is checked on the first 10 layers of the same
+full-size configuration.
 """
 
 import numpy as np
@@ -144,6 +146,11 @@ def test_pooling_streamed_equals_resident_bitexact(lib, mode, ranks, rank):
         assert np.all(np.isfinite(ref[0]))
         assert np.array_equal(got[0].view(np.uint32), ref[0].view(np.uint32))
         assert np.array_equal(got[1], ref[1]) and np.array_equal(got[2], ref[2])
+        # and the pooled, streamed step against the oracle (the layout of the
+        # weights changes nothing in what a step computes, §4.1)
+        want, _, _, _ = st.run_oracle(range(st.batch), steps=3)
+        want_exact, _, _, _ = st.run_oracle(range(st.batch), steps=3, round_bf16=False)
+        _check_hidden(got[0].astype(np.float64), want, want_exact, f"pooled {mode} d={ranks} r={rank}, 3 steps")
         # back to whole-layer staging with no owned layers: still the same bits
         st.reset()
         st.dec.set_pooling(lib.SIDP_POOL_LAYER, 0, 0)
@@ -239,6 +246,113 @@ def test_decode_before_pool_loaded_is_state_error(lib):
         assert e.value.code == lib.SIDP_ESTATE
     finally:
         dec.close()
+
+
+def test_injected_hip_error_poisons_handle(lib):
+    """The error contract: a HIP runtime failure is returned as SIDP_EHIP with
+    the runtime's code kept for sidp_last_hip_error, and the handle is then
+    poisoned: every later call returns SIDP_ESTATE, sidp_destroy still frees
+    it. The failure is injected on the host; no GPU work faults."""
+    cfg = synth.get_config("tiny_layer", num_layers=2)
+    st = Stack(cfg)
+    try:
+        h = st.dec.h
+        s = torch.cuda.current_stream().cuda_stream
+        mb = st.bt.shape[1]
+        args = (h, st.hidden.data_ptr(), st.positions.data_ptr(), st.bt.data_ptr(), mb, st.batch, 0, s, None)
+        assert lib.raw_call("sidp_decode_step", *args) == lib.SIDP_OK
+        st.dec.sync()
+        assert lib.raw_call("sidp_debug_inject_hip_error", h, 0) == lib.SIDP_EINVAL
+        assert lib.raw_call("sidp_debug_inject_hip_error", h, 700) == lib.SIDP_OK
+        assert lib.raw_call("sidp_decode_step", *args) == lib.SIDP_EHIP
+        assert lib.sidp_last_hip_error(h) == 700
+        for name, a in [("sidp_decode_step", args), ("sidp_sync", (h,)), ("sidp_set_pooling", (h, 0, 0, 0)),
+                        ("sidp_set_fill_tiles", (h, 25, 0, 0)), ("sidp_debug_inject_hip_error", (h, 1))]:
+            assert lib.raw_call(name, *a) == lib.SIDP_ESTATE, name
+        torch.cuda.synchronize()
+    finally:
+        st.close()
+
+
+def test_reload_layer_between_streamed_steps_bitexact(lib):
+    """Loading new weights into a layer between streamed steps restarts the
+    slot ring, so the next step computes every layer from its new blob: the
+    same bits as resident steps with the same reload, even though the slots
+    held (and the copy stream was filling) the old blobs."""
+    cfg = _small_stack_cfg(num_layers=3)
+    st = Stack(cfg, gains="random", regions=2, reserve=3)
+    try:
+        copy = torch.cuda.Stream()
+        w_new = synth.layer_weights(cfg, 0, seed=5, device="cuda", gains="random")
+        outs = {}
+        for name, flags in [("resident", lib.SIDP_RESIDENT), ("streamed", lib.SIDP_STREAMED)]:
+            st.reset()
+            for l in range(3):
+                st.dec.load_layer(l, synth.layer_weights(cfg, l, seed=0, device="cuda", gains="random"))
+            torch.cuda.synchronize()
+            st.dec.step(st.hidden, st.positions, st.bt, flags, copy=copy)
+            st.dec.sync()
+            st.dec.load_layer(0, w_new)
+            torch.cuda.synchronize()
+            st.dec.step(st.hidden, st.positions + 1, st.bt, flags, copy=copy)
+            st.dec.sync()
+            outs[name] = st.hidden.cpu().numpy().copy()
+        assert np.all(np.isfinite(outs["resident"]))
+        assert np.array_equal(outs["streamed"].view(np.uint32), outs["resident"].view(np.uint32))
+    finally:
+        st.close()
+
+
+def test_steps_on_changing_compute_streams_bitexact(lib):
+    """Consecutive steps issued on different compute streams (and copy
+    streams) are ordered by the library: the result equals the same steps on
+    one stream, bit for bit."""
+    cfg = _small_stack_cfg(num_layers=4, batch=160, num_phys_blocks=None)
+    st = Stack(cfg, gains="random", regions=2, reserve=4)
+    try:
+        outs = {}
+        for name in ("one", "many"):
+            st.reset()
+            streams = [torch.cuda.Stream() for _ in range(4)]
+            # inputs made on the current stream are complete before other streams read them
+            pos = [st.positions + s for s in range(4)]
+            torch.cuda.synchronize()
+            for s in range(4):
+                cs = torch.cuda.current_stream() if name == "one" else streams[s]
+                cp = streams[(s + 1) % 4] if name == "many" else streams[1]
+                st.dec.step(st.hidden, pos[s], st.bt, lib.SIDP_STREAMED | lib.SIDP_DEBUG_DELAY, compute=cs, copy=cp)
+            st.dec.sync()
+            torch.cuda.synchronize()
+            outs[name] = st.hidden.cpu().numpy().copy()
+        assert np.all(np.isfinite(outs["one"]))
+        assert np.array_equal(outs["many"].view(np.uint32), outs["one"].view(np.uint32))
+    finally:
+        st.close()
+
+
+@pytest.mark.parametrize("tiles", [(0, 0, 0), (25, 8, 8), (60, 2, 4), (100, 4, 2)])
+def test_fill_tiles_bitexact(lib, tiles):
+    """Any split of the fill into its two tiles, and any loads in flight, gives
+    the resident bits, with poisoned slots and delayed fills."""
+    cfg = _small_stack_cfg(num_layers=3)
+    st = Stack(cfg, gains="random", regions=2, reserve=2)
+    try:
+        copy = torch.cuda.Stream()
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
+        st.dec.sync()
+        ref = st.hidden.cpu().numpy().copy()
+        st.reset()
+        lib.sidp_set_fill_tiles(st.dec.h, *tiles)
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED | lib.SIDP_DEBUG_POISON | lib.SIDP_DEBUG_DELAY,
+                    copy=copy)
+        st.dec.sync()
+        assert np.array_equal(st.hidden.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+        for bad in [(-1, 0, 0), (101, 0, 0), (25, 3, 0), (25, 0, 16)]:
+            with pytest.raises(lib.SidpError) as e:
+                lib.sidp_set_fill_tiles(st.dec.h, *bad)
+            assert e.value.code == lib.SIDP_EINVAL
+    finally:
+        st.close()
 
 
 # ------------------------------------------------------------------ full-size shapes, sampled rows
@@ -338,11 +452,34 @@ def test_llama70b_stack80_first10_layers_parity(lib):
         st.close()
 
 
+def test_llama70b_ffn_only_pooling_owned_layers_sampled_rows(lib):
+    """FFN-only pooling on the full-size 70B shape at B=256: four layers,
+    layers 1 and 3 owned by this rank (computed from the pool), layers 0 and 2
+    streaming only their FFN part through the slots; sampled rows from both
+    128-row blocks against the oracle."""
+    st = _stack80(4, regions=2)
+    try:
+        st.dec.set_pooling(lib.SIDP_POOL_FFN, 2, 1)
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        rows = [0, 200]
+        got = st.hidden.double().cpu().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
+        _check_hidden(got, want, want_exact, "70B shape, FFN-only pooling, owned layers", tight=False)
+    finally:
+        st.close()
+
+
 @pytest.mark.slow
 def test_llama70b_stack80_full_depth(lib):
-    """All 80 layers at B=256: streamed and resident weights give identical
-    bits; sampled rows stay within 2x the drift between the oracle's own bf16
-    and exact evaluations at this depth."""
+    """All 80 layers at B=256 (the benchmark's workload): streamed and resident
+    weights give identical bits, and rows 0, 127 and 255 (both 128-row blocks
+    of the projections) are checked against both oracle evaluations, computed
+    in this run. The bar: the GPU's per-row error against the exact oracle is
+    at most max(2e-2, 2 x the bf16-rounding oracle's own error against the
+    exact oracle) for that row; at this depth the latter alone is about 3e-2,
+    since bf16 storage drifts over 80 layers whoever evaluates it."""
     st = _stack80(80)
     try:
         st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
@@ -352,10 +489,14 @@ def test_llama70b_stack80_full_depth(lib):
         st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
         st.dec.sync()
         assert torch.equal(st.hidden.cpu(), streamed)
-        rows = [255]
+        rows = [0, 127, 255]
         got = streamed.double().numpy()[rows]
-        want, _, _, _ = st.run_oracle(rows)
-        e = row_rel_err(got, want)
-        assert np.all(np.isfinite(got)) and e.max() <= 6.5e-2, e
+        want_bf, want_ex = st.run_oracle_both(rows)
+        e_bf, e_ex, drift = row_rel_err(got, want_bf), row_rel_err(got, want_ex), row_rel_err(want_bf, want_ex)
+        for r, a, b, c in zip(rows, e_bf, e_ex, drift):
+            print(f"row {r}: GPU vs bf16 oracle {a:.3e}, GPU vs exact oracle {b:.3e}, "
+                  f"oracle bf16 vs exact {c:.3e}", flush=True)
+        assert np.all(np.isfinite(got))
+        assert np.all(e_ex <= np.maximum(BAR, 2.0 * drift)), (e_ex, drift)
     finally:
         st.close()
