@@ -369,6 +369,24 @@ int sidp_pack_gate_up(const void *w_gate, const void *w_up, int32_t f, int32_t k
 int sidp_linear(sidp_handle *h, const void *x, int32_t m, int32_t k, const void *packed, int32_t n,
                 int32_t epilogue, const void *bias, const float *residual, void *out, void *stream);
 
+/* ---- the projection without allocation ----
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation): the projection of
+ * sidp_linear without a handle, on the current device. Same arguments,
+ * layouts and results as sidp_linear, bit for bit (the same kernels and the
+ * same split of K); m <= 4096. Allocates nothing: the split-K partials go to
+ * a scratch array of SIDP_NOALLOC_SCRATCH_BYTES that the library's code
+ * object holds in each device's memory from module load until the process
+ * ends (32 MiB: the most any split needs on a 256-CU MI355X). SIDP_EINVAL
+ * for bad arguments and when this shape's partials would outgrow the scratch
+ * (possible only on a device with more CUs); SIDP_EHIP if the runtime fails.
+ * Every call on a device shares that device's scratch, and nothing in it must
+ * start at zero (each split writes its partials before they are summed);
+ * calls that overlap in time on one device (on different streams) race. */
+#define SIDP_NOALLOC_SCRATCH_BYTES (32u << 20)
+int sidp_linear_noalloc(const void *x, int32_t m, int32_t k, const void *packed, int32_t n, int32_t epilogue,
+                        const void *bias, const float *residual, void *out, void *stream);
+
 /* Slot mapping (K9): slots[b] = bt[b][p / bs] * bs + p % bs, p = positions[b];
  * device int32 arrays. An entry out of range yields -1 and latches
  * SIDP_EINVAL for sidp_sync. */

@@ -50,7 +50,7 @@ EXPORTED = [
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_peak_shift_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
     "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select", "sidp_mode_update",
-    "sidp_set_fill_tiles", "sidp_debug_inject_hip_error",
+    "sidp_set_fill_tiles", "sidp_debug_inject_hip_error", "sidp_linear_noalloc",
 ]
 
 SIDP_CAS_MAX_REPLICAS = 16
@@ -125,6 +125,7 @@ _sigs = {
     "sidp_pack_linear": (ctypes.c_int, [_P, _I, _I, _P, _P]),
     "sidp_pack_gate_up": (ctypes.c_int, [_P, _P, _I, _I, _P, _P]),
     "sidp_linear": (ctypes.c_int, [_P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _P]),
+    "sidp_linear_noalloc": (ctypes.c_int, [_P, _I, _I, _P, _I, _I, _P, _P, _P, _P]),
     "sidp_slot_mapping": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P]),
     "sidp_rope_append": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _P, _P, _I, _P, _P]),
     "sidp_attention": (ctypes.c_int, [_P, _P, _I, _P, _P, _I, _I, _P, _P]),
@@ -318,6 +319,11 @@ def sidp_pack_gate_up(w_gate, w_up, f, k, packed, stream=None):
 def sidp_linear(h, x, m, k, packed, n, epilogue, bias, residual, out, stream=None):
     _check(_lib.sidp_linear(h, _ptr(x), m, k, _ptr(packed), n, epilogue, _ptr(bias), _ptr(residual), _ptr(out),
                             _stream(stream)), "sidp_linear")
+
+
+def sidp_linear_noalloc(x, m, k, packed, n, epilogue, bias, residual, out, stream=None):
+    _check(_lib.sidp_linear_noalloc(_ptr(x), m, k, _ptr(packed), n, epilogue, _ptr(bias), _ptr(residual), _ptr(out),
+                                    _stream(stream)), "sidp_linear_noalloc")
 
 
 def sidp_slot_mapping(h, positions, block_tables, max_blocks_per_seq, batch, slots, stream=None):
