@@ -72,7 +72,7 @@ def algorithmic_work(cfg, B, seq_total, fill_bytes):
         "gate_up": (2 * F * H * 2 + B * H * 2 + B * F * 2, 2 * B * 2 * F * H),
         # and the down projection's reduction writes the next layer's attention-norm output
         "down": (H * F * 2 + B * F * 2 + 2 * B * H * 4 + H * 2 + B * H * 2, 2 * B * H * F),
-        "fill": (fill_bytes, 0),  # per launch: 2 x fill_bytes over the layer's two tiles
+        "fill": (fill_bytes, 0),  # read + write 2 x fill_bytes per streamed layer, over its fill launches
         "wait_fill": (0, 0),
     }
     return w
@@ -102,6 +102,30 @@ def measured_traffic(kernel):
             return None
         return rec["traffic_bytes_per_launch"] if h.hexdigest() == rec["source_sha256"] else None
     return None
+
+
+def cpu_baseline_one_core(cfg, weights_for_layer, kv_rows, x_rows, pos_rows, tabs_rows):
+    """The oracle on one layer of the same sample, with the calling thread
+    pinned to one host core and BLAS limited to one thread; returns tokens/s
+    extrapolated to the full stack, the core, and the seconds it took."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    prev = os.sched_getaffinity(0)
+    core = min(prev)
+    k_np, v_np = kv_rows
+    with threadpool_limits(limits=1):
+        os.sched_setaffinity(0, {core})
+        try:
+            t0 = time.perf_counter()
+            x = oracle.decode_layer(x_rows.copy(), weights_for_layer(0), cfg, k_np.copy(), v_np.copy(), pos_rows,
+                                    tabs_rows, True)
+            dt = time.perf_counter() - t0
+        finally:
+            os.sched_setaffinity(0, prev)
+    assert np.all(np.isfinite(x))
+    return x.shape[0] / (dt * cfg["num_layers"]), core, dt
 
 
 def cpu_baseline(cfg, weights_for_layer, kv_rows, x_rows, pos_rows, tabs_rows, n_layers_sample):
@@ -287,6 +311,11 @@ def main():
                          "engines of --batch lanes (implies --bth)")
     ap.add_argument("--bth", action="store_true",
                     help="also profile B_th: the smallest batch whose layer time covers one layer's weight fetch")
+    ap.add_argument("--fill-split", type=int, default=25, help="percent of a layer's fill in its first tile")
+    ap.add_argument("--fill-loads", type=int, nargs=2, default=[0, 0], metavar=("A", "B"),
+                    help="16-byte loads in flight per fill lane in the two tiles (0 0: the batch default)")
+    ap.add_argument("--whole-fill-wait", action="store_true",
+                    help="a layer waits for its whole fill before it starts (default: each kernel waits for its part)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-regions", type=int, default=0, help="0: fill the HBM left after the pool")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -393,6 +422,8 @@ def main():
         flags |= sidp.SIDP_COPY_SDMA
 
     dec.set_pooling(sidp.SIDP_POOL_FFN if args.pooling == "ffn" else sidp.SIDP_POOL_LAYER, args.ranks, args.rank)
+    sidp.sidp_set_fill_tiles(dec.h, args.fill_split, args.fill_loads[0], args.fill_loads[1],
+                             0 if args.whole_fill_wait else 1)
     for i in range(args.warmup):
         dec.step(hidden, pos, bt, flags, compute=compute, copy=copy_stream)
     dec.sync()
@@ -400,6 +431,7 @@ def main():
     log(f"warmup {args.warmup} steps done")
 
     seq_total = int(ctx.sum()) + B
+    streamed_layers = L - sum(1 for l in range(L) if args.ranks > 0 and l % args.ranks == args.rank)
     fill_bytes = staged_bytes(cfg, layer_bytes, args.pooling)
     work = algorithmic_work(cfg, B, seq_total, fill_bytes)
 
@@ -410,6 +442,8 @@ def main():
                 continue
             avg = ms / n
             byts, flops = work[name]
+            if name == "fill":  # a layer's fill is several launches that together read and write it once
+                byts = int(2 * fill_bytes * streamed_layers * steps / n)
             row = {"launches": n, "ms_per_launch": round(avg, 5), "ms_per_step": round(ms / steps, 4)}
             if avg > 0 and byts > 0:
                 row.update({
@@ -480,10 +514,18 @@ def main():
     if not args.no_cpu_baseline:
         val, threads, dt = cpu_baseline(cfg, lambda l: keep_w[l], kv_rows, x0[sample_rows].double().cpu().numpy(),
                                         ctx[sample_rows], np.asarray(tabs_rows), sample_layers)
+        val1, core, dt1 = cpu_baseline_one_core(cfg, lambda l: keep_w[l], kv_rows,
+                                                x0[sample_rows].double().cpu().numpy(), ctx[sample_rows],
+                                                np.asarray(tabs_rows))
         cpu = {"value": round(val, 3), "unit": "tok/s", "cores": threads, "kind": "oracle",
                "sample": f"{sample_layers} of {L} layers for {len(sample_rows)} of {B} sequences (full contexts), "
-                         f"float64 with bf16 storage rounding; {dt:.1f}s; tok/s = rows / (s per layer x {L})"}
-        log(f"oracle baseline: {val:.3f} tok/s over {dt:.1f}s with {threads} BLAS threads")
+                         f"float64 with bf16 storage rounding; {dt:.1f}s; tok/s = rows / (s per layer x {L})",
+               "host_cpus": os.cpu_count(), "blas_threads": threads,
+               "one_core": {"value": round(val1, 4), "unit": "tok/s", "cores": 1, "core": core,
+                            "sample": f"layer 0 for the same {len(sample_rows)} sequences, this thread pinned to "
+                                      f"host core {core}, one BLAS thread; {dt1:.1f}s"}}
+        log(f"oracle baseline: {val:.3f} tok/s over {dt:.1f}s with {threads} BLAS threads "
+            f"({os.cpu_count()} host CPUs); one core: {val1:.4f} tok/s over {dt1:.1f}s")
 
     cas = cas_leg(dec, cfg, args.cas, args.cas_rows, compute) if args.cas > 0 else None
     bth = None
@@ -501,6 +543,8 @@ def main():
             "parallelism": "single GPU", "mode": args.mode, "copy": args.copy, "kv_regions": R,
             "layer_bytes": layer_bytes, "pooling": args.pooling, "staged_bytes": fill_bytes,
             "owned_layers": sum(1 for l in range(L) if args.ranks > 0 and l % args.ranks == args.rank),
+            "fill": {"first_tile_percent": args.fill_split, "loads": args.fill_loads,
+                     "waits": "whole fill" if args.whole_fill_wait else "per part"},
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -59,7 +59,7 @@ extern "C" {
                                 /* DMA engines, no compute units                                 */
                                 /* default: a background fill kernel sized to run beside compute */
 #define SIDP_DEBUG_POISON  0x10 /* before each fill, write NaN bytes over the slot */
-#define SIDP_DEBUG_DELAY   0x20 /* before each fill, spin ~200 us on the copy stream */
+#define SIDP_DEBUG_DELAY   0x20 /* before each fill launch, spin ~200 us on the copy stream */
 #define SIDP_TIMING        0x40 /* bracket each kernel class with HIP events (sidp_timing_collect) */
 
 /* ---- kernel classes timed under SIDP_TIMING ---- */
@@ -187,7 +187,8 @@ int sidp_kv_attach(sidp_handle *h, void *k_cache, void *v_cache, int32_t num_phy
  *  compute      stream for the layer kernels.
  *  copy         stream for slot fills (STREAMED only; must differ from compute).
  * STREAMED keeps a ring of 2 slots: layer g (counted across calls) computes
- * from slot g % 2 after waiting for its fill; the fill of layer g + 2 waits
+ * from slot g % 2, each of its kernels after the part of the fill it reads
+ * has landed (see sidp_plan); the fill of layer g + 2 waits
  * for layer g's compute to release the slot. The copy stream thus runs two
  * layers ahead, into the next call's first layers too. RESIDENT and STREAMED
  * give bit-identical results (the paper's modes change only where weights
@@ -240,11 +241,16 @@ int sidp_set_pooling(sidp_handle *h, int32_t mode, int32_t ranks, int32_t rank);
  * released, the rest once the previous layer's attention half has been
  * issued, so that it runs beside that layer's projections. loads_a and
  * loads_b are the 16-byte loads each lane of the fill kernel keeps in flight
- * in the two tiles (2, 4 or 8; 0 = the default for the step's batch: 4 and 2
- * from 128 rows up, 8 and 4 below). Defaults: 25, 0, 0. Takes effect from the
- * next decode step. SIDP_EINVAL for a percent outside [0, 100] or another
- * load count. */
-int sidp_set_fill_tiles(sidp_handle *h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b);
+ * in the two tiles (2, 4 or 8; 0 = the default for the step's batch: 8 and 4
+ * below 128 rows; 4 and 4 from 128 to 383 rows with part waits; else 4 and
+ * 2). part_waits = 1: each kernel that reads
+ * the slot waits only for the fill launch holding its weights (see
+ * sidp_plan), so the compute stream does not stall on the rest of the fill;
+ * 0: a layer waits for its whole fill before its first kernel. Defaults:
+ * 25, 0, 0, 1. Takes effect from the next decode step. SIDP_EINVAL for a
+ * percent outside [0, 100], another load count, or part_waits not 0 or 1. */
+int sidp_set_fill_tiles(sidp_handle *h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b,
+                        int32_t part_waits);
 
 /* ---- Compute-as-a-Service, owner side ----
  * §4.3: in the small-batch tail, non-owner replicas send their FFN inputs to
@@ -280,9 +286,15 @@ int sidp_cas_ffn(sidp_handle *h, int32_t layer, int32_t n_replicas, const void *
  * g + 1 is copied into the other slot as two tiles (§4.2 "tensor tiles", each
  * with its notification): tile A once layer g - 1 has released the slot, tile
  * B once layer g's attention half has been issued, so that it runs beside
- * layer g's projections. Each op is 3 int32 {kind, g, slot}; kinds:
+ * layer g's projections. Each kernel that reads the slot waits only for the
+ * tile holding the last byte it reads (unless sidp_set_fill_tiles asks for
+ * whole-fill waits): the attention half for the bytes below W_o (op 2), the
+ * O projection and its fused norm for those below the gate/up weights, the
+ * FFN for the whole fill (both inside op 5). Each op is 3 int32
+ * {kind, g, slot}; kinds:
  *   0 copy tile A of layer g          1 copy tile B of layer g, then mark filled
- *   2 compute waits for the fill      3 attention half of layer g
+ *   2 compute waits for the attention half's part of the fill
+ *   3 attention half of layer g
  *   4 mark attention half issued      5 projection half of layer g
  *   6 mark slot released              7 copy stream waits for the release
  *   8 copy stream waits for the attention half

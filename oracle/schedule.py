@@ -30,10 +30,13 @@ its neighbours in layer order.
 Operations, in host issue order, as (kind, g, slot):
   ("fill_a", g, s)     copy tile A of layer g mod L into slot s
   ("fill_b", g, s)     copy tile B, then notify "filled"
-  ("wait_fill", g, s)  compute waits for layer g's "filled"
+  ("wait_fill", g, s)  compute waits for the part of layer g's fill that its
+                       attention half reads
   ("attn", g, s)       attention half of layer g
   ("mid", g, s)        compute notifies that the attention half is issued
-  ("proj", g, s)       projection half of layer g
+  ("proj", g, s)       projection half of layer g (each projection first
+                       waits for the part of the fill holding its weights;
+                       the last of them waits for "filled")
   ("done", g, s)       compute notifies that slot s is free
   ("wait_done", g, s)  copy waits for layer g's "done"
   ("wait_mid", g, s)   copy waits for layer g's "mid"

@@ -116,7 +116,7 @@ _sigs = {
     "sidp_plan": (ctypes.c_int, [_I, _I, _I, _I, _PI, _PI]),
     "sidp_peak_shift_plan": (ctypes.c_int, [_I, _I, _I, _PI, _PI]),
     "sidp_set_pooling": (ctypes.c_int, [_P, _I, _I, _I]),
-    "sidp_set_fill_tiles": (ctypes.c_int, [_P, _I, _I, _I]),
+    "sidp_set_fill_tiles": (ctypes.c_int, [_P, _I, _I, _I, _I]),
     "sidp_debug_inject_hip_error": (ctypes.c_int, [_P, _I]),
     "sidp_cas_ffn": (ctypes.c_int, [_P, _I, _I, ctypes.POINTER(_P), _PI, ctypes.POINTER(_P), _P]),
     "sidp_timing_select": (ctypes.c_int, [_P, ctypes.c_uint32]),
@@ -281,8 +281,8 @@ def sidp_set_pooling(h, mode, ranks=0, rank=0):
     _check(_lib.sidp_set_pooling(h, mode, ranks, rank), "sidp_set_pooling")
 
 
-def sidp_set_fill_tiles(h, first_tile_percent=25, loads_a=0, loads_b=0):
-    _check(_lib.sidp_set_fill_tiles(h, first_tile_percent, loads_a, loads_b), "sidp_set_fill_tiles")
+def sidp_set_fill_tiles(h, first_tile_percent=25, loads_a=0, loads_b=0, part_waits=1):
+    _check(_lib.sidp_set_fill_tiles(h, first_tile_percent, loads_a, loads_b, part_waits), "sidp_set_fill_tiles")
 
 
 def sidp_debug_inject_hip_error(h, hip_error):

@@ -356,8 +356,10 @@ size_t packed_bytes(int n, int k) { return (size_t)round_up(n, 64) * round_up(k,
 // The kernels address the packed weights and the activations through 32-bit
 // buffer offsets.
 bool gemm_fits(int m, int n_cols_packed, int k) {
+  // the activations stay below 2^31 bytes, so the out-of-range offset 2^31
+  // that rows past M and k past K read through lies past them
   constexpr size_t kLimit = (size_t)1 << 32;
-  return packed_bytes(n_cols_packed, k) < kLimit && (size_t)m * round_up(k, 64) * 2 < kLimit;
+  return packed_bytes(n_cols_packed, k) < kLimit && (size_t)m * round_up(k, 64) * 2 < ((size_t)1 << 31);
 }
 
 

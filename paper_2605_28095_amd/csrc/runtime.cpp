@@ -32,6 +32,7 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
 constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
 constexpr int kFillSmallBatch = 128;   // below this many rows the fill runs with more loads in flight
+constexpr int kFillLongBatch = 384;    // from this many rows the projections outlast a gentle tile B
 constexpr int kBurstGrid = 512;        // workgroups of the whole-chip burst copy (SIDP_COPY_BURST)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -188,6 +189,11 @@ struct sidp_handle {
   float *rope_cos = nullptr, *rope_sin = nullptr;
   uint32_t* err = nullptr;
   hipEvent_t filled[kSlots] = {}, consumed[kSlots] = {}, mid[kSlots] = {};
+  // A slot's fill is two launches on the copy stream, tiles A and B;
+  // tile_a[slot] is recorded after tile A, filled[slot] after tile B. Each
+  // kernel that reads the slot waits only for the tile holding the last byte
+  // it reads, so the rest of the fill may still run beside it.
+  hipEvent_t tile_a[kSlots] = {};
   // Recorded on the compute stream after each call that uses the handle's
   // buffers; a later call on another stream waits for it first.
   hipEvent_t work_done = nullptr;
@@ -201,6 +207,9 @@ struct sidp_handle {
   // Below kFillSmallBatch rows a layer computes in less time than its fill takes,
   // so both parts press harder there. 0: that per-batch default; else a fixed count.
   int fill_loads_a = 0, fill_loads_b = 0;
+  // 1: each kernel that reads a slot waits only for the fill launch holding
+  // its weights; 0: the layer waits for its whole fill before it starts
+  int part_waits = 1;
   int step_batch = 0;  // rows of the decode step being issued
   // pooling: which part of a layer is staged, and which layers this rank owns
   int pool_mode = SIDP_POOL_LAYER;
@@ -265,6 +274,7 @@ static void free_device(sidp_handle* h) {
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; i++) {
     if (h->filled[i]) (void)hipEventDestroy(h->filled[i]);
+    if (h->tile_a[i]) (void)hipEventDestroy(h->tile_a[i]);
     if (h->consumed[i]) (void)hipEventDestroy(h->consumed[i]);
     if (h->mid[i]) (void)hipEventDestroy(h->mid[i]);
   }
@@ -342,6 +352,7 @@ int sidp_create(const sidp_config* cfg, sidp_handle** out) {
   if (hipMemcpy(h->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) return fail(SIDP_EHIP);
   for (int i = 0; i < kSlots; i++) {
     if (hipEventCreateWithFlags(&h->filled[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
+    if (hipEventCreateWithFlags(&h->tile_a[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->consumed[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
     if (hipEventCreateWithFlags(&h->mid[i], hipEventDisableTiming) != hipSuccess) return fail(SIDP_EHIP);
   }
@@ -603,15 +614,40 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   return hipSuccess;
 }
 
+// The compute stream's waits for the tiles of a slot fill (streamed layers
+// only): before a kernel that reads the slot, the tile holding the last byte
+// it reads.
+struct SlotWaits {
+  sidp_handle* h;
+  int slot;         // -1: weights read in place, no wait
+  size_t tile_a_end;  // end of tile A in the blob (tile B ends at the staged range's end)
+  int done = -1;    // the last tile already waited for (0: A, 1: B)
+};
+
+// Waits (on s) until the bytes of the slot below `need_end` have landed.
+static hipError_t wait_slot_bytes(SlotWaits* w, size_t need_end, hipStream_t s) {
+  if (!w || w->slot < 0) return hipSuccess;
+  const int tile = need_end <= w->tile_a_end ? 0 : 1;
+  if (tile <= w->done) return hipSuccess;
+  hipError_t e;
+  if ((e = time_begin(w->h, SIDP_K_WAIT_FILL, s)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(s, tile ? w->h->filled[w->slot] : w->h->tile_a[w->slot], 0)) != hipSuccess) return e;
+  w->done = tile;
+  return time_end(w->h, SIDP_K_WAIT_FILL, s);
+}
+
 // The projection half of a layer (O + residual, norm, gate/up + SwiGLU,
 // down + residual).
 // `wa` holds the layer's attention part (W_o), `wf` its FFN part; both are
 // the same blob unless only the FFN part is staged.
 static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wa, const uint8_t* wf, int layer, float* hidden, int B,
-                                hipStream_t s) {
+                                hipStream_t s, SlotWaits* waits = nullptr) {
   const sidp_config& c = h->cfg;
   const BlobLayout& L = h->blob;
   const int H = c.hidden, QD = c.num_q_heads * c.head_dim;
+  hipError_t e;
+  // W_o and the FFN norm gain lie below the gate/up weights
+  if ((e = wait_slot_bytes(waits, L.w_gu, s)) != hipSuccess) return e;
   // a7 + a8: O projection + residual (in place on the fp32 residual stream),
   // then the RMSNorm before the FFN, fused into the split-K reduction
   LinearCall oc = linear_call(h, h->o, B, QD, wa + L.w_o, H, SIDP_EPI_RESID, nullptr, hidden, hidden);
@@ -619,7 +655,10 @@ static hipError_t run_proj_half(sidp_handle* h, const uint8_t* wa, const uint8_t
   oc.norm_eps = c.rms_eps;
   oc.norm_out = h->h;
   TIMED(h, SIDP_K_O, s, launch_linear(oc, s));
-  // a9: gate/up projection + SwiGLU
+  // a9: gate/up projection + SwiGLU; the FFN's weights (gate/up, then down)
+  // take one wait, for the whole fill: a second wait inside the FFN gained
+  // nothing measurable and its timing brackets cost about 1 ms per step
+  if ((e = wait_slot_bytes(waits, L.total, s)) != hipSuccess) return e;
   TIMED(h, SIDP_K_GATE_UP, s,
         launch_linear(linear_call(h, h->h, B, H, wf + L.w_gu, c.ffn_dim, SIDP_EPI_SWIGLU, nullptr, nullptr, h->act),
                       s));
@@ -664,17 +703,26 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   hipError_t e;
   if (part_a && (flags & SIDP_DEBUG_POISON))  // the whole slot, unstaged parts included
     if ((e = launch_poison(dst, lb, cp)) != hipSuccess) return e;
-  if (part_a && (flags & SIDP_DEBUG_DELAY))
-    if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
   if (hi <= lo) return hipSuccess;
+  if (flags & SIDP_DEBUG_DELAY)  // every launch lands late: a missing wait on any part reads poison
+    if ((e = launch_spin(kDelayTicks, cp)) != hipSuccess) return e;
   if ((e = time_begin(h, SIDP_K_FILL, cp)) != hipSuccess) return e;
   if (flags & SIDP_COPY_MEMCPY) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDevice, cp);
   else if (flags & SIDP_COPY_SDMA) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDeviceNoCU, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, kBurstGrid, cp);
   else {
+    // Defaults: below kFillSmallBatch rows a layer computes in less time than
+    // its fill takes, so both tiles press hard. From there up tile A keeps 4
+    // loads per lane in flight; tile B keeps 4 when each kernel waits only for
+    // its part and the batch is under kFillLongBatch rows (tile B then has to
+    // land within the projections, or its tail and the next tile A run into
+    // the attention), else 2: from kFillLongBatch rows the projections last
+    // long enough for 2, and when the layer waits for its whole fill any more
+    // slows the projections beside it more than the stall it saves.
     const bool small = h->step_batch < kFillSmallBatch;
     const int la = h->fill_loads_a ? h->fill_loads_a : (small ? 8 : 4);
-    const int lb = h->fill_loads_b ? h->fill_loads_b : (small ? 4 : 2);
+    const int lb = h->fill_loads_b ? h->fill_loads_b
+                                    : (small || (h->part_waits && h->step_batch < kFillLongBatch) ? 4 : 2);
     e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? la : lb, cp);
   }
   if (e != hipSuccess) return e;
@@ -728,6 +776,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
   const size_t lb = h->blob.total;
   size_t st_lo, st_mid, st_hi;
   staged_range(h, &st_lo, &st_mid, &st_hi);
+  SlotWaits waits{h, -1, 0};
   const bool ffn_only = h->pool_mode == SIDP_POOL_FFN;
   for (const RingOp& op : ops) {
     const uint8_t* slot = op.slot >= 0 ? h->slots + (size_t)op.slot * lb : nullptr;
@@ -736,16 +785,20 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
     switch (op.kind) {
       case OP_FILL_A:
         HIPCHK(h, issue_fill(h, op.g, op.slot, st_lo, st_mid, flags, cp));
+        HIPCHK(h, hipEventRecord(h->tile_a[op.slot], cp));
         break;
       case OP_FILL_B:
         HIPCHK(h, issue_fill(h, op.g, op.slot, st_mid, st_hi, flags, cp));
         HIPCHK(h, hipEventRecord(h->filled[op.slot], cp));
         break;
       case OP_WAIT_FILL:
-        // under SIDP_TIMING the interval around the wait is the compute stall on the fill
-        HIPCHK(h, time_begin(h, SIDP_K_WAIT_FILL, cs));
-        HIPCHK(h, hipStreamWaitEvent(cs, h->filled[op.slot], 0));
-        HIPCHK(h, time_end(h, SIDP_K_WAIT_FILL, cs));
+        // The compute stream waits for the part of the fill the attention half
+        // reads (its gains, bias and W_qkv, below W_o; nothing when only the
+        // FFN part is staged); the projections wait for theirs in turn. Under
+        // SIDP_TIMING each wait is bracketed: the compute stall on the fill.
+        waits = SlotWaits{h, op.slot, st_mid};
+        if (!h->part_waits) HIPCHK(h, wait_slot_bytes(&waits, h->blob.total, cs));
+        else if (!ffn_only) HIPCHK(h, wait_slot_bytes(&waits, h->blob.w_o, cs));
         break;
       case OP_ATTN:
         HIPCHK(h, run_attn_half(h, ffn_only ? own : slot, layer, hidden, positions, block_tables, max_blocks_per_seq,
@@ -755,7 +808,7 @@ int sidp_decode_step(sidp_handle* h, float* hidden, const int32_t* positions, co
         HIPCHK(h, hipEventRecord(h->mid[op.slot], cs));
         break;
       case OP_PROJ:
-        HIPCHK(h, run_proj_half(h, ffn_only ? own : slot, slot, layer, hidden, batch, cs));
+        HIPCHK(h, run_proj_half(h, ffn_only ? own : slot, slot, layer, hidden, batch, cs, &waits));
         break;
       case OP_DONE:
         HIPCHK(h, hipEventRecord(h->consumed[op.slot], cs));
@@ -844,12 +897,15 @@ int sidp_set_pooling(sidp_handle* h, int32_t mode, int32_t ranks, int32_t rank) 
   return SIDP_OK;
 }
 
-int sidp_set_fill_tiles(sidp_handle* h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b) {
+int sidp_set_fill_tiles(sidp_handle* h, int32_t first_tile_percent, int32_t loads_a, int32_t loads_b,
+                        int32_t part_waits) {
   if (!h) return SIDP_EINVAL;
   if (h->poisoned) return SIDP_ESTATE;
   auto loads_ok = [](int32_t n) { return n == 0 || n == 2 || n == 4 || n == 8; };
-  if (first_tile_percent < 0 || first_tile_percent > 100 || !loads_ok(loads_a) || !loads_ok(loads_b))
+  if (first_tile_percent < 0 || first_tile_percent > 100 || !loads_ok(loads_a) || !loads_ok(loads_b) ||
+      (part_waits != 0 && part_waits != 1))
     return SIDP_EINVAL;
+  h->part_waits = part_waits;
   h->fill_pct = first_tile_percent;
   h->fill_loads_a = loads_a;
   h->fill_loads_b = loads_b;

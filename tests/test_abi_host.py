@@ -113,7 +113,7 @@ def test_null_handle_calls_are_rejected():
     assert sidp.raw_call("sidp_destroy", None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_decode_step", None, None, None, None, 1, 1, 0, None, None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_plan", 0, 1, 0, 0, None, None) == sidp.SIDP_EINVAL
-    assert sidp.raw_call("sidp_set_fill_tiles", None, 25, 0, 0) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_set_fill_tiles", None, 25, 0, 0, 1) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_debug_inject_hip_error", None, 1) == sidp.SIDP_EINVAL
 
 

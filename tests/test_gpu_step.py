@@ -267,7 +267,7 @@ def test_injected_hip_error_poisons_handle(lib):
         assert lib.raw_call("sidp_decode_step", *args) == lib.SIDP_EHIP
         assert lib.sidp_last_hip_error(h) == 700
         for name, a in [("sidp_decode_step", args), ("sidp_sync", (h,)), ("sidp_set_pooling", (h, 0, 0, 0)),
-                        ("sidp_set_fill_tiles", (h, 25, 0, 0)), ("sidp_debug_inject_hip_error", (h, 1))]:
+                        ("sidp_set_fill_tiles", (h, 25, 0, 0, 1)), ("sidp_debug_inject_hip_error", (h, 1))]:
             assert lib.raw_call(name, *a) == lib.SIDP_ESTATE, name
         torch.cuda.synchronize()
     finally:
@@ -330,7 +330,7 @@ def test_steps_on_changing_compute_streams_bitexact(lib):
         st.close()
 
 
-@pytest.mark.parametrize("tiles", [(0, 0, 0), (25, 8, 8), (60, 2, 4), (100, 4, 2)])
+@pytest.mark.parametrize("tiles", [(0, 0, 0, 1), (25, 8, 8, 1), (60, 2, 4, 1), (100, 4, 2, 1), (25, 4, 2, 0), (5, 2, 2, 0)])
 def test_fill_tiles_bitexact(lib, tiles):
     """Any split of the fill into its two tiles, and any loads in flight, gives
     the resident bits, with poisoned slots and delayed fills."""
@@ -347,7 +347,7 @@ def test_fill_tiles_bitexact(lib, tiles):
                     copy=copy)
         st.dec.sync()
         assert np.array_equal(st.hidden.cpu().numpy().view(np.uint32), ref.view(np.uint32))
-        for bad in [(-1, 0, 0), (101, 0, 0), (25, 3, 0), (25, 0, 16)]:
+        for bad in [(-1, 0, 0, 1), (101, 0, 0, 1), (25, 3, 0, 1), (25, 0, 16, 1), (25, 0, 0, 2)]:
             with pytest.raises(lib.SidpError) as e:
                 lib.sidp_set_fill_tiles(st.dec.h, *bad)
             assert e.value.code == lib.SIDP_EINVAL
