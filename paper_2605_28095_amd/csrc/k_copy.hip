@@ -97,10 +97,11 @@ static hipError_t launch_fill_u(const void* src, void* dst, size_t bytes, int nu
   return hipGetLastError();
 }
 
-// The kernel addresses a launch's range with 32-bit buffer offsets, so a
-// range past 1 GiB is filled by several launches of at most 1 GiB each, back
-// to back on the stream (same engine, same grid).
-constexpr size_t kFillChunk = (size_t)1 << 30;
+// The kernel addresses a launch's range through a buffer resource whose size
+// field is a signed 32-bit count, so a range of 2 GiB or more is filled by
+// several launches just under 2 GiB each, back to back on the stream (same
+// engine, same grid).
+constexpr size_t kFillChunk = ((size_t)1 << 31) - 4096;
 
 hipError_t launch_fill_bg(const void* src, void* dst, size_t bytes, int num_cus, int loads, hipStream_t s) {
   if (bytes % 16) return hipErrorInvalidValue;  // slot ranges are 256-byte aligned
