@@ -235,6 +235,19 @@ __global__ void __launch_bounds__(64 * W, W > 4 ? 1 : 2) k_gemm(GemmArgs a) {
         acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, as_bf16x8(w[kh * 2 + 1]), acc[m][1], 0, 0, 0);
       }
     }
+    if constexpr (MF == 4) {
+      // Scheduling hint (mask 0x100 = LDS reads, 0x008 = MFMAs): read each
+      // activation fragment two MFMA pairs ahead of its use, so that an LDS
+      // read's latency hides behind matrix work instead of stalling the pipe:
+      // 3 reads, then (2 MFMAs, 1 read) x 5, then the last 6 MFMAs.
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+      for (int i = 0; i < 5; i++) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    }
   };
 
   // Every load of the k loop is issued on every path (a wait count can only
