@@ -27,6 +27,11 @@
 //    or by the kernel that consumes the result (the RoPE/KV-append kernel for
 //    QKV, the residual + RMSNorm reduction for O and down; LinearCall's
 //    defer_reduce and norm_out select this).
+//  * k_gemm_lw is the same contraction with 256-row workgroups whose weight
+//    tiles are staged once per CU in LDS (direct-to-LDS loads) and shared by
+//    both 128-row halves. It halves the weight loads per flop but needs twice
+//    the splits at a given batch; launch_linear takes it only where k_gemm
+//    would leave a quarter of the CUs idle (use_lds_weights).
 #include "common.h"
 #include "internal.h"
 
@@ -128,6 +133,46 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 
 __device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Writes one wave's tile: rows row0 + [0, 32 MF), the 64 packed columns of
+// group ng; acc[m][nf] holds the 32x32 block (m, nf) in the MFMA's layout
+// (register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32).
+template <int MF, int EPI, bool PARTIAL>
+__device__ __forceinline__ void store_tile(const GemmArgs& a, const f32x16_t (&acc)[MF][2], int row0, int ng,
+                                           int split, int lane) {
+  const int NP = a.NG * 64;
+#pragma unroll
+  for (int m = 0; m < MF; m++) {
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      const int row = row0 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      if (row >= a.M) continue;
+      if (PARTIAL) {
+        float* dst = a.ws + ((int64_t)split * a.M + row) * NP + ng * 64 + (lane & 31);
+        dst[0] = acc[m][0][r];
+        dst[32] = acc[m][1][r];
+      } else if (EPI == SIDP_EPI_SWIGLU) {
+        const int f = ng * 32 + (lane & 31);
+        if (f < a.N)
+          ((uint16_t*)a.out)[(int64_t)row * a.N + f] = f2bf(silu_f(acc[m][0][r]) * acc[m][1][r]);
+      } else {
+#pragma unroll
+        for (int nf = 0; nf < 2; nf++) {
+          const int n = ng * 64 + nf * 32 + (lane & 31);
+          if (n >= a.N) continue;
+          const int64_t o = (int64_t)row * a.N + n;
+          if (EPI == SIDP_EPI_BF16) {
+            float v = acc[m][nf][r];
+            if (a.bias) v += bf2f(a.bias[n]);
+            ((uint16_t*)a.out)[o] = f2bf(v);
+          } else {
+            ((float*)a.out)[o] = a.resid ? a.resid[o] + acc[m][nf][r] : acc[m][nf][r];
+          }
+        }
+      }
+    }
+  }
 }
 
 // One workgroup: W waves (4, or 8 for wide unsplit launches). Wave wn
@@ -272,45 +317,170 @@ __global__ void __launch_bounds__(64 * W, W > 4 ? 1 : 2) k_gemm(GemmArgs a) {
   load_w_half(kt0, 1, whi);
   store_x(lds0);
   __syncthreads();
-  for (int kt = kt0; kt < kt1; kt += 2) {
+  // Pairs of k-tiles, then an odd last tile outside the loop: an exit from
+  // the middle of the unrolled body would give the loop header a second
+  // predecessor on which the first step's weight loads are still pending,
+  // and the header would wait for them on every iteration.
+  int kt = kt0;
+  for (; kt + 1 < kt1; kt += 2) {
     step(kt, lds0, lds1, wlo, whi, nlo, nhi);
-    if (kt + 1 >= kt1) break;
     step(kt + 1, lds1, lds0, nlo, nhi, wlo, whi);
   }
+  if (kt < kt1) step(kt, lds0, lds1, wlo, whi, nlo, nhi);
 
   if (!active) return;
-  const int NP = a.NG * 64;
+  store_tile<MF, EPI, PARTIAL>(a, acc, row0, ng, split, lane);
+}
+
+// LDS-staged weights. One 8-wave workgroup per CU covers 256 rows x 256
+// columns: waves 0-3 take rows 0-127 and waves 4-7 rows 128-255 of the same
+// four column groups. Each weight fragment of a stage is fetched once per
+// workgroup, straight into LDS by direct-to-LDS buffer loads (no VGPR round
+// trip), and read there by the two waves that use it; the 256-row activation
+// tile is staged through LDS as in k_gemm. A stage is 32 k (two MFMA k steps);
+// two stages (2 x 32 KB) are in LDS at once, which leaves room beside a CU's
+// slot-fill workgroup. Each stage buffer is its own LDS array, so the compiler
+// can tell that reading the current stage does not depend on the direct loads
+// landing in the other one.
+constexpr int kLwRows = 256;                 // rows per workgroup
+constexpr int kLwBK = 32;                    // k per stage
+constexpr int kLwA = kLwRows * kLwBK;        // bf16 elements of a stage's activations (16 KB)
+constexpr int kLwW = 4 * 4 * kFragElems;     // 4 groups x 4 fragments (16 KB)
+
+// s_waitcnt vmcnt(0): expcnt and lgkmcnt at their no-wait maxima (7, 15)
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
+template <int EPI, bool PARTIAL>
+__global__ void __launch_bounds__(512, 1) k_gemm_lw(GemmArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint16_t lw_a0[kLwA];
+  __shared__ __attribute__((aligned(1024))) uint16_t lw_a1[kLwA];
+  __shared__ __attribute__((aligned(1024))) uint16_t lw_w0[kLwW];
+  __shared__ __attribute__((aligned(1024))) uint16_t lw_w1[kLwW];
+
+  // workgroup id -> (column tile, split, row block), row blocks 8 ids apart (as k_gemm)
+  int pair, mblk;
+  {
+    const int L = blockIdx.x;
+    const int per_group = 8 * a.mblocks;
+    const int r = L % per_group;
+    pair = (L / per_group) * 8 + (r % 8);
+    mblk = r / 8;
+    if (pair >= a.tiles * a.splits) return;
+  }
+  const int split = pair % a.splits;
+  const int tile = pair / a.splits;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int half = wave >> 2, g = wave & 3;
+  const int ng = tile * 4 + g;
+  const bool active = ng < a.NG;
+  const int row0 = mblk * kLwRows + half * 128;  // this wave's rows
+  // the split's k range in 64-wide k-tiles (as k_gemm), walked in 32-wide stages
+  const int KT = a.KP / kBK;
+  const int st0 = 2 * (int)((int64_t)split * KT / a.splits);
+  const int st1 = 2 * (int)((int64_t)(split + 1) * KT / a.splits);
+
+  const __amdgpu_buffer_rsrc_t xr_rsrc = make_rsrc(a.x, (uint32_t)((size_t)a.M * a.K * 2));
+  const __amdgpu_buffer_rsrc_t wr_rsrc = make_rsrc(a.w, (uint32_t)((size_t)a.NG * a.KP * 64 * 2));
+
+  // Activations: stage rows r = 0..255, 16-byte chunks c = 0..3 (8 k each);
+  // thread t stages chunks t and t + 512. In LDS a row is 64 bytes and chunk
+  // c sits at slot c ^ ((r >> 2) & 3): the 16 rows one LDS cycle serves for a
+  // fragment read (one chunk each) then fall on 16 distinct 16-byte bank groups.
+  int x_row[2], x_cc[2];
 #pragma unroll
-  for (int m = 0; m < MF; m++) {
+  for (int i = 0; i < 2; i++) {
+    const int ci = threadIdx.x + i * 512;
+    x_row[i] = ci >> 2;
+    x_cc[i] = ci & 3;
+  }
+  u32x4_t xs[2];
+  auto load_x = [&](int st) {
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int row = row0 + m * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-      if (row >= a.M) continue;
-      if (PARTIAL) {
-        float* dst = a.ws + ((int64_t)split * a.M + row) * NP + ng * 64 + (lane & 31);
-        dst[0] = acc[m][0][r];
-        dst[32] = acc[m][1][r];
-      } else if (EPI == SIDP_EPI_SWIGLU) {
-        const int f = ng * 32 + (lane & 31);
-        if (f < a.N)
-          ((uint16_t*)a.out)[(int64_t)row * a.N + f] = f2bf(silu_f(acc[m][0][r]) * acc[m][1][r]);
-      } else {
+    for (int i = 0; i < 2; i++) {
+      const int row = mblk * kLwRows + x_row[i];
+      const int k = st * kLwBK + x_cc[i] * 8;
+      const bool in = row < a.M && k < a.K;
+      const uint32_t off = in ? (uint32_t)(((size_t)row * a.K + k) * 2) : kOutOfRange;
+      xs[i] = buf_load16(xr_rsrc, off, 0);
+    }
+  };
+  auto store_x = [&](uint16_t* lds) {
 #pragma unroll
-        for (int nf = 0; nf < 2; nf++) {
-          const int n = ng * 64 + nf * 32 + (lane & 31);
-          if (n >= a.N) continue;
-          const int64_t o = (int64_t)row * a.N + n;
-          if (EPI == SIDP_EPI_BF16) {
-            float v = acc[m][nf][r];
-            if (a.bias) v += bf2f(a.bias[n]);
-            ((uint16_t*)a.out)[o] = f2bf(v);
-          } else {
-            ((float*)a.out)[o] = a.resid ? a.resid[o] + acc[m][nf][r] : acc[m][nf][r];
-          }
-        }
+    for (int i = 0; i < 2; i++) {
+      const int r = x_row[i];
+      *(u32x4_t*)(lds + r * kLwBK + ((x_cc[i] ^ ((r >> 2) & 3)) << 3)) = xs[i];
+    }
+  };
+  // Weights of stage st: k-tile st / 2, k steps 2 (st % 2) and + 1, so bytes
+  // [4 KB (st % 2), + 4 KB) of each group's 8 KB piece: fragments (k step,
+  // column half) in packed order. Wave (half, g) fetches fragments 2 half and
+  // 2 half + 1 of group g into LDS fragment slot 4 g + f (1 KB each; lane l's
+  // 16 bytes land at 16 l). A group past NG re-reads group 0 (its waves skip
+  // the MFMAs).
+  const uint32_t w_lane = (uint32_t)lane * 16u;
+  const uint32_t w_group = (uint32_t)(active ? ng : 0) * 8192u;
+  auto load_w = [&](int st, uint16_t* lds) {
+    const uint32_t soff = (uint32_t)(st >> 1) * (uint32_t)a.NG * 8192u + w_group + (uint32_t)(st & 1) * 4096u;
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int f = half * 2 + j;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          wr_rsrc, (__attribute__((address_space(3))) void*)(lds + (g * 4 + f) * kFragElems), 16, w_lane,
+          soff + (uint32_t)f * 1024u, 0, 0);
+    }
+  };
+
+  f32x16_t acc[4][2];
+#pragma unroll
+  for (int m = 0; m < 4; m++)
+#pragma unroll
+    for (int n = 0; n < 2; n++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) acc[m][n][r] = 0.f;
+
+  const int arow = lane & 31;
+  auto mma_stage = [&](const uint16_t* xa, const uint16_t* wl) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ks++) {
+      const bf16x8_t b0 = as_bf16x8(*(const u32x4_t*)(wl + (g * 4 + ks * 2 + 0) * kFragElems + lane * 8));
+      const bf16x8_t b1 = as_bf16x8(*(const u32x4_t*)(wl + (g * 4 + ks * 2 + 1) * kFragElems + lane * 8));
+      const int cc = ks * 2 + (lane >> 5);
+#pragma unroll
+      for (int m = 0; m < 4; m++) {
+        const int r = half * 128 + m * 32 + arow;
+        const bf16x8_t af = as_bf16x8(*(const u32x4_t*)(xa + r * kLwBK + ((cc ^ ((r >> 2) & 3)) << 3)));
+        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b0, acc[m][0], 0, 0, 0);
+        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b1, acc[m][1], 0, 0, 0);
       }
     }
+  };
+
+  // Stage st computes from (xa, wl) while stage st + 1 is fetched into (xn,
+  // wn); every path issues the same loads (the prefetch past the split's last
+  // stage re-reads that stage).
+  auto step = [&](int st, const uint16_t* xa, const uint16_t* wl, uint16_t* xn, uint16_t* wn) {
+    const int sn = min(st + 1, st1 - 1);
+    load_x(sn);
+    load_w(sn, wn);
+    if (active) mma_stage(xa, wl);
+    store_x(xn);
+    wait_vm0();  // this wave's direct-to-LDS loads have landed before the barrier
+    __syncthreads();
+  };
+  load_x(st0);
+  load_w(st0, lw_w0);
+  store_x(lw_a0);
+  wait_vm0();
+  __syncthreads();
+  int st = st0;
+  for (; st + 1 < st1; st += 2) {
+    step(st, lw_a0, lw_w0, lw_a1, lw_w1);
+    step(st + 1, lw_a1, lw_w1, lw_a0, lw_w0);
   }
+  if (st < st1) step(st, lw_a0, lw_w0, lw_a1, lw_w1);
+
+  if (!active) return;
+  store_tile<4, EPI, PARTIAL>(a, acc, row0, ng, split, lane);
 }
 
 // Sum split-K partials in split order and apply the epilogue.
@@ -376,11 +546,32 @@ bool gemm_fits(int m, int n_cols_packed, int k) {
 }
 
 
+static int splits_for(int tiles, int mblocks, int KT, int num_cus);
+
+// Whether a projection runs on k_gemm_lw (256-row workgroups, weights staged
+// in LDS) rather than k_gemm (128-row blocks, weights into registers). Alone
+// at B = 256 the LDS-staged kernel is slower on all four 70B projections
+// (QKV 53 against 51 us, O 46 against 40, down 143-148 against 129-136,
+// gate/up 318-335 against 284-309, its reductions 5 us slower with twice the
+// splits); it wins where k_gemm would run a single unsplit round on under
+// three quarters of the CUs, as QKV at 512 rows does (160 workgroups: 128-132
+// us against 95-97 plus a 16 us reduction on 240).
+static bool use_lds_weights(int M, int NG, int K, int num_cus) {
+  if (M <= 128 || K % 64) return false;
+  const int tiles = (NG + kWaves - 1) / kWaves, mblocks = (M + 127) / 128;
+  return splits_for(tiles, mblocks, K / kBK, num_cus) == 1 && (int64_t)tiles * mblocks * 4 < 3 * (int64_t)num_cus;
+}
+
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus) {
   const int NG = round_up(n_cols_packed, 64) / 64;
+  const bool lw = use_lds_weights(M, NG, K, num_cus);
   const int tiles = (NG + kWaves - 1) / kWaves;
-  const int mblocks = (M + 127) / 128;
+  const int mblocks = lw ? (M + kLwRows - 1) / kLwRows : (M + 127) / 128;
   const int KT = round_up(K, 64) / kBK;
+  return splits_for(tiles, mblocks, KT, num_cus);
+}
+
+static int splits_for(int tiles, int mblocks, int KT, int num_cus) {
   const int base = tiles * mblocks;
   // As many splits as keep the grid at most one 4-wave workgroup per CU (two
   // fit): each split writes fp32 partials for all M x N outputs, and at decode
@@ -449,11 +640,22 @@ static hipError_t launch_mf(GemmArgs a, hipStream_t s) {
 }
 
 template <int EPI, bool P>
+static hipError_t launch_lw(GemmArgs a, hipStream_t s) {
+  a.mblocks = (a.M + kLwRows - 1) / kLwRows;
+  a.tiles = (a.NG + 3) / 4;
+  const int pairs = a.tiles * a.splits;
+  const int grid = (pairs + 7) / 8 * 8 * a.mblocks;
+  k_gemm_lw<EPI, P><<<grid, 512, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int EPI, bool P>
 static hipError_t launch_epi(const GemmArgs& a, hipStream_t s, int wide = 0) {
   if constexpr (!P) {
     if (wide == 7) return launch_mf<4, EPI, P, 7>(a, s);
     if (wide == 8) return launch_mf<4, EPI, P, 8>(a, s);
   }
+  if (wide == -1) return launch_lw<EPI, P>(a, s);
   if (a.M <= 32) return launch_mf<1, EPI, P>(a, s);
   if (a.M <= 64) return launch_mf<2, EPI, P>(a, s);
   return launch_mf<4, EPI, P>(a, s);
@@ -489,8 +691,8 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   // that the model counts as busy); ties go to the wider one. A 70B-shaped
   // gate/up (896 column groups) gets 7 waves at 256 rows, exactly 256
   // workgroups; a 924-group one 8.
-  int wide = 0;
-  if (a.splits == 1 && c.m > 64) {
+  int wide = use_lds_weights(c.m, a.NG, c.k, c.num_cus) ? -1 : 0;
+  if (wide == 0 && a.splits == 1 && c.m > 64) {
     const int64_t mb = (c.m + 127) / 128, cus = std::max(1, c.num_cus);
     const int64_t n4 = (a.NG + 3) / 4 * mb, n7 = (a.NG + 6) / 7 * mb, n8 = (a.NG + 7) / 8 * mb;
     int64_t best = (n4 + 2 * cus - 1) / (2 * cus) * 8;
@@ -505,7 +707,7 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
     if (e != hipSuccess || !fuse_norm) return e;
     return launch_rmsnorm((const float*)c.out, c.norm_gain, c.norm_eps, c.norm_out, a.M, a.N, s);
   }
-  e = launch_epi<SIDP_EPI_BF16, true>(a, s);  // partials only; epilogue in the reduction
+  e = launch_epi<SIDP_EPI_BF16, true>(a, s, wide);  // partials only; epilogue in the reduction
   if (e != hipSuccess || c.defer_reduce) return e;
   if (fuse_norm && reduce_resid_norm_fits(a.N))
     return launch_reduce_resid_norm(a.ws, a.splits, a.M, a.NG * 64, a.N, (float*)c.out, c.norm_gain, c.norm_eps,

@@ -66,6 +66,12 @@ LINEAR_CASES = [
     (128, 3072, 1024, 1, False),   # three k-tiles per split: whole rounds of the three-deep ring only
     (100, 256, 45056, 0, True),    # enough column tiles for one split
     (200, 512, 28672, 2, False),   # SwiGLU without a split past 64 rows: the gate/up launch of a decode step
+    # 256-row workgroups with LDS-staged weights (k_gemm alone would run one unsplit round on 160 of
+    # 256 CUs): split partials reduced with the bias, with SwiGLU, and in place on the residual with
+    # ragged rows and columns (groups past N idle)
+    (512, 512, 10240, 0, True),
+    (512, 512, 5120, 2, False),
+    (400, 512, 9000, 1, False),
 ]
 
 
