@@ -205,7 +205,8 @@ struct sidp_handle {
   // KV append (latency-bound, spare bandwidth), so it may press harder; part B
   // runs beside the projections, which lose more than the fill gains when it does.
   // Below kFillSmallBatch rows a layer computes in less time than its fill takes,
-  // so both parts press harder there. 0: that per-batch default; else a fixed count.
+  // so both parts press harder there. 0: the per-batch default of issue_fill;
+  // else a fixed count.
   int fill_loads_a = 0, fill_loads_b = 0;
   // 1: each kernel that reads a slot waits only for the fill launch holding
   // its weights; 0: the layer waits for its whole fill before it starts
@@ -711,18 +712,18 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   else if (flags & SIDP_COPY_SDMA) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDeviceNoCU, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, kBurstGrid, cp);
   else {
-    // Defaults: below kFillSmallBatch rows a layer computes in less time than
-    // its fill takes, so both tiles press hard. From there up tile A keeps 4
-    // loads per lane in flight; tile B keeps 4 when each kernel waits only for
-    // its part and the batch is under kFillLongBatch rows (tile B then has to
-    // land within the projections, or its tail and the next tile A run into
-    // the attention), else 2: from kFillLongBatch rows the projections last
-    // long enough for 2, and when the layer waits for its whole fill any more
-    // slows the projections beside it more than the stall it saves.
-    const bool small = h->step_batch < kFillSmallBatch;
-    const int la = h->fill_loads_a ? h->fill_loads_a : (small ? 8 : 4);
-    const int lb = h->fill_loads_b ? h->fill_loads_b
-                                    : (small || (h->part_waits && h->step_batch < kFillLongBatch) ? 4 : 2);
+    // Defaults: tile A keeps 8 loads per lane in flight and tile B 4 below
+    // kFillSmallBatch rows (a layer computes in less time than its fill
+    // takes), and below kFillLongBatch rows when each kernel waits only for
+    // its part (tile B then has to land within the projections, or its tail
+    // and the next tile A run into the attention; at 256 rows 8 and 4 ran
+    // 1.3% faster than 4 and 4). Otherwise 4 and 2: from kFillLongBatch rows
+    // the projections last long enough for a gentler fill (4 and 2 beat 8 and
+    // 2 or 8 and 4 at 512 rows), and when the layer waits for its whole fill
+    // any more slows the projections beside it more than the stall it saves.
+    const bool press = h->step_batch < kFillSmallBatch || (h->part_waits && h->step_batch < kFillLongBatch);
+    const int la = h->fill_loads_a ? h->fill_loads_a : (press ? 8 : 4);
+    const int lb = h->fill_loads_b ? h->fill_loads_b : (press ? 4 : 2);
     e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? la : lb, cp);
   }
   if (e != hipSuccess) return e;
