@@ -283,10 +283,10 @@ __device__ __forceinline__ int seq_parts(const AttnCall& a, int b) {
 }
 
 // Item i of the work list is (entry i / Hkv of the plan, KV head i % Hkv).
-// Two 4-wave workgroups per CU (the register cap keeps a wave at 248 VGPRs so
-// that a fill wave still fits beside two of them on a SIMD).
+// Two 4-wave workgroups per CU; a wave holds 218 VGPRs (224 allocated), so
+// two of them and a slot-fill wave (at most 48) fit in a SIMD's 512.
 template <int D>
-__global__ void __launch_bounds__(256, 2) __attribute__((amdgpu_num_vgpr(124))) k_attn(AttnCall a) {
+__global__ void __launch_bounds__(256, 2) k_attn(AttnCall a) {
   constexpr int KK = D / 32, JD = D / 16;
   extern __shared__ __attribute__((aligned(16))) float smem_f[];
   float* s_m = smem_f;                             // [4][16]

@@ -30,13 +30,17 @@ __global__ void __launch_bounds__(256) k_copy16(const f4v_t* __restrict__ src, f
 
 // Background slot fill: runs beside the layer kernels instead of ahead of
 // them. One 4-wave workgroup per CU with few VGPRs per wave and scalar buffer
-// bases, so a fill wave fits in the registers a projection or attention SIMD
-// leaves free (those kernels use at most 232 of a lane's 512 registers with
-// two waves per SIMD). The 81 KB of LDS it requests and never touches keeps
-// two fill workgroups off one CU (2 x 81 KB > 160 KB) while one still fits
-// beside two projection (2 x 32 KB) or two attention (2 x 34 KB) workgroups,
-// so the fill never claims the resources a layer kernel needs. U 16-byte
-// loads per lane are in flight per iteration.
+// bases: 12, 24 or 48 allocated for 2, 4 or 8 loads per lane. Beside two
+// attention waves (224 each) or two projection waves (up to 240 each, the
+// 7-wave gate/up) on a SIMD there is room for the 2- and 4-load fill waves;
+// the 8-load one, used only for the first tile of a layer, fits beside
+// attention and beside the split projections (one wave per SIMD), which is
+// what that tile runs beside. The 81 KB of LDS it requests and never touches
+// keeps two fill workgroups off one CU (2 x 81 KB > 160 KB) while one still
+// fits beside two projection (2 x 32 KB), two attention (2 x 34 KB) or one
+// LDS-staged projection (64 KB) workgroups, so the fill never claims the
+// resources a layer kernel needs. U 16-byte loads per lane are in flight per
+// iteration.
 constexpr int kFillLdsBytes = 81 * 1024;
 constexpr uint32_t kFillRsrcWord3 = 0x00020000u;
 
@@ -62,18 +66,17 @@ __device__ __forceinline__ void fill_body(const uint8_t* __restrict__ src, uint8
   }
 }
 
-// The register caps are literals (the attribute takes no expression).
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(16)))
+__global__ void __launch_bounds__(256)
 k_fill_bg2(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
   extern __shared__ uint8_t fill_lds_reserve[];
   fill_body<2>(src, dst, n16);
 }
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(24)))
+__global__ void __launch_bounds__(256)
 k_fill_bg4(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
   extern __shared__ uint8_t fill_lds_reserve[];
   fill_body<4>(src, dst, n16);
 }
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_num_vgpr(40)))
+__global__ void __launch_bounds__(256)
 k_fill_bg8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, uint32_t n16) {
   extern __shared__ uint8_t fill_lds_reserve[];
   fill_body<8>(src, dst, n16);
