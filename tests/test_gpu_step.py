@@ -452,6 +452,31 @@ def test_llama70b_stack80_first10_layers_parity(lib):
         st.close()
 
 
+def test_llama70b_b512_two_layers_parity(lib):
+    """Two layers of the 70B shape at B=512, where the QKV projection runs on
+    the LDS-staged-weight kernel (256-row workgroups, three splits) and the
+    RoPE/KV-append kernel reduces its partials: streamed and resident weights
+    give identical bits, and rows from both 256-row blocks and both 128-row
+    halves of a block (0, 300, 511) match the oracle."""
+    cfg = synth.get_config("llama70b_stack80", num_layers=2)
+    st = Stack(cfg, batch=512, keep_weights=False, regions=2)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        streamed = st.hidden.cpu().clone()
+        st.reset()
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
+        st.dec.sync()
+        assert torch.equal(st.hidden.cpu(), streamed)
+        rows = [0, 300, 511]
+        got = streamed.double().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
+        _check_hidden(got, want, want_exact, "70B shape at B=512, 2 layers", tight=False)
+    finally:
+        st.close()
+
+
 def test_llama70b_ffn_only_pooling_owned_layers_sampled_rows(lib):
     """FFN-only pooling on the full-size 70B shape at B=256: four layers,
     layers 1 and 3 owned by this rank (computed from the pool), layers 0 and 2
