@@ -36,6 +36,9 @@ DESCR = {
     "qwen3_32b_layer": "Qwen3-32B-shaped single layer",
     "tiny_layer": "tiny single layer",
 }
+# Depth of the model a workload is shaped like: shallower stacks also report
+# the per-layer time and the tok/s projected to the model's depth.
+MODEL_LAYERS = {"llama70b_stack80": 80, "qwen25_72b_stack8": 80, "llama70b_layer": 80, "qwen3_32b_layer": 64}
 
 
 def log(msg):
@@ -474,14 +477,20 @@ def main():
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
+    # an event after every step on the compute stream gives the per-step spread
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     e0.record(compute)
     for i in range(args.steps):
         dec.step(hidden, pos, bt, flags | sidp.SIDP_TIMING, compute=compute, copy=copy_stream)
+        if i + 1 < args.steps:
+            ev[i].record(compute)
     e1.record(compute)
     torch.cuda.synchronize()
     dec.sync()
     wall = time.perf_counter() - w0
     ms_total = e0.elapsed_time(e1)
+    marks = [e0] + ev[:args.steps - 1] + [e1]
+    step_ms = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     ms_per_step = ms_total / args.steps
     value = B / (ms_per_step / 1e3)
     dk = kernel_table(sidp.sidp_timing_collect(dec.h), args.steps)[dom]
@@ -551,9 +560,17 @@ def main():
         "kernels": kernels,
         "kernels_note": (f"per-class HIP-event timing of {breakdown_steps} steps run before the timed region with every "
                          "class bracketed; the timed region brackets only the roofline kernel's class"),
+        "step_ms": {"p10": round(float(np.percentile(step_ms, 10)), 3), "median": round(float(np.median(step_ms)), 3),
+                    "p90": round(float(np.percentile(step_ms, 90)), 3),
+                    "tok_s_at_median": round(B / (float(np.median(step_ms)) / 1e3), 2)},
         "resident_ms_per_step": round(resident_ms, 3) if resident_ms else None,
         "fill_stall_ms_per_step": kernels["wait_fill"]["ms_per_step"] if "wait_fill" in kernels else None,
     }
+    depth = MODEL_LAYERS.get(args.workload)
+    if depth and depth != L:
+        out["projection"] = {"t_layer_ms": round(ms_per_step / L, 4), "model_layers": depth,
+                             "projected_tok_s": round(B / (ms_per_step / L * depth / 1e3), 2),
+                             "note": "a projection: this stack's per-layer step time times the model's depth"}
     if cas:
         out["cas"] = cas
     if bth:
