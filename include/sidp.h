@@ -241,8 +241,8 @@ int sidp_set_pooling(sidp_handle *h, int32_t mode, int32_t ranks, int32_t rank);
  * released, the rest once the previous layer's attention half has been
  * issued, so that it runs beside that layer's projections. loads_a and
  * loads_b are the 16-byte loads each lane of the fill kernel keeps in flight
- * in the two tiles (2, 4 or 8; 0 = the default for the step's batch: 8 and 4
- * below 128 rows, and below 384 rows with part waits; else 4 and 2).
+ * in the two tiles (2, 4 or 8; 0 = the default for the step's batch: 8 and 8
+ * below 160 rows; 8 and 4 below 384 rows with part waits; else 4 and 2).
  * part_waits = 1: each kernel that reads
  * the slot waits only for the fill launch holding its weights (see
  * sidp_plan), so the compute stream does not stall on the rest of the fill;

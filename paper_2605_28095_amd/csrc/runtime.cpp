@@ -31,7 +31,7 @@ constexpr int kSlots = 2;
 constexpr size_t kAlign = 256;
 constexpr int64_t kDelayTicks = 20000;  // 200 us of the 100 MHz constant clock
 constexpr int kFillPartAPercent = 25;  // share of a layer's fill issued before its predecessor's attention
-constexpr int kFillSmallBatch = 128;   // below this many rows the fill runs with more loads in flight
+constexpr int kFillSmallBatch = 160;   // below this many rows both fill tiles keep 8 loads per lane in flight
 constexpr int kFillLongBatch = 384;    // from this many rows the projections outlast a gentle tile B
 constexpr int kBurstGrid = 512;        // workgroups of the whole-chip burst copy (SIDP_COPY_BURST)
 
@@ -712,18 +712,21 @@ static hipError_t issue_fill(sidp_handle* h, int64_t g, int slot, size_t lo, siz
   else if (flags & SIDP_COPY_SDMA) e = hipMemcpyAsync(dst + lo, src + lo, hi - lo, hipMemcpyDeviceToDeviceNoCU, cp);
   else if (flags & SIDP_COPY_BURST) e = launch_copy(src + lo, dst + lo, hi - lo, kBurstGrid, cp);
   else {
-    // Defaults: tile A keeps 8 loads per lane in flight and tile B 4 below
-    // kFillSmallBatch rows (a layer computes in less time than its fill
-    // takes), and below kFillLongBatch rows when each kernel waits only for
-    // its part (tile B then has to land within the projections, or its tail
-    // and the next tile A run into the attention; at 256 rows 8 and 4 ran
-    // 1.3% faster than 4 and 4). Otherwise 4 and 2: from kFillLongBatch rows
-    // the projections last long enough for a gentler fill (4 and 2 beat 8 and
-    // 2 or 8 and 4 at 512 rows), and when the layer waits for its whole fill
-    // any more slows the projections beside it more than the stall it saves.
-    const bool press = h->step_batch < kFillSmallBatch || (h->part_waits && h->step_batch < kFillLongBatch);
+    // Defaults: below kFillSmallBatch rows a layer computes in less time than
+    // its fill takes, so both tiles keep 8 loads per lane in flight (at 16,
+    // 64 and 128 rows 1-2% faster than 8 and 4; at 192 rows 5% slower).
+    // From there tile A keeps 8 and tile B 4 below kFillLongBatch rows when
+    // each kernel waits only for its part (tile B then has to land within the
+    // projections, or its tail and the next tile A run into the attention; at
+    // 256 rows 8 and 4 ran 1.3% faster than 4 and 4). Otherwise 4 and 2: from
+    // kFillLongBatch rows the projections last long enough for a gentler fill
+    // (4 and 2 beat 8 and 4 at 384 and 512 rows), and when the layer waits for
+    // its whole fill any more slows the projections beside it more than the
+    // stall it saves.
+    const bool small = h->step_batch < kFillSmallBatch;
+    const bool press = small || (h->part_waits && h->step_batch < kFillLongBatch);
     const int la = h->fill_loads_a ? h->fill_loads_a : (press ? 8 : 4);
-    const int lb = h->fill_loads_b ? h->fill_loads_b : (press ? 4 : 2);
+    const int lb = h->fill_loads_b ? h->fill_loads_b : (small ? 8 : press ? 4 : 2);
     e = launch_fill_bg(src + lo, dst + lo, hi - lo, h->num_cus, part_a ? la : lb, cp);
   }
   if (e != hipSuccess) return e;
