@@ -365,6 +365,22 @@ int sidp_debug_inject_hip_error(sidp_handle *h, int32_t hip_error);
  * n multiple of 4. */
 int sidp_rmsnorm(const float *x, const void *gain, float eps, void *out, int32_t rows, int32_t n, void *stream);
 
+/* The launch sidp_linear, sidp_linear_noalloc and the decode step make for
+ * the projection out[m, n] = x[m, k] W[n, k]^T with `epilogue` on a GPU with
+ * `num_cus` compute units (host only, no device call). kernel: 0 = weights
+ * streamed into registers by each 128-row block, 1 = 256-row workgroups whose
+ * weight tiles are staged once in LDS (taken where kernel 0 would run one
+ * unsplit round on under three quarters of the CUs). waves: per workgroup (4,
+ * 7 or 8). rows_per_workgroup: 32, 64, 128 or 256. splits: the split-K count
+ * (fp32 partials reduced in split order). workgroups: the grid launched.
+ * ws_bytes: bytes of partials (0 without a split). All outputs host,
+ * caller-owned. SIDP_EINVAL for a null output, m < 1, n < 1, k < 8 or not a
+ * multiple of 8, n or k above 2^24, num_cus < 1, an unknown epilogue, or
+ * sizes past the kernels' 32-bit buffer offsets. */
+int sidp_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t num_cus, int32_t *kernel,
+                     int32_t *waves, int32_t *rows_per_workgroup, int32_t *splits, int32_t *workgroups,
+                     uint64_t *ws_bytes);
+
 /* Bytes of a matrix [n, k] packed for sidp_linear (n padded to 64, k to 64). */
 size_t sidp_packed_bytes(int32_t n, int32_t k);
 /* Packs W (device bf16 [n, k], nn.Linear layout) into `packed`

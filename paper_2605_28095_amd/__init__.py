@@ -50,7 +50,7 @@ EXPORTED = [
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_peak_shift_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
     "sidp_timing_collect", "sidp_set_pooling", "sidp_cas_ffn", "sidp_timing_select", "sidp_mode_update",
-    "sidp_set_fill_tiles", "sidp_debug_inject_hip_error", "sidp_linear_noalloc",
+    "sidp_set_fill_tiles", "sidp_debug_inject_hip_error", "sidp_linear_noalloc", "sidp_linear_plan",
 ]
 
 SIDP_CAS_MAX_REPLICAS = 16
@@ -126,6 +126,8 @@ _sigs = {
     "sidp_pack_gate_up": (ctypes.c_int, [_P, _P, _I, _I, _P, _P]),
     "sidp_linear": (ctypes.c_int, [_P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _P]),
     "sidp_linear_noalloc": (ctypes.c_int, [_P, _I, _I, _P, _I, _I, _P, _P, _P, _P]),
+    "sidp_linear_plan": (ctypes.c_int, [_I, _I, _I, _I, _I, _PI, _PI, _PI, _PI, _PI,
+                                        ctypes.POINTER(ctypes.c_uint64)]),
     "sidp_slot_mapping": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P]),
     "sidp_rope_append": (ctypes.c_int, [_P, _P, _P, _P, _I, _I, _P, _P, _I, _P, _P]),
     "sidp_attention": (ctypes.c_int, [_P, _P, _I, _P, _P, _I, _I, _P, _P]),
@@ -244,6 +246,18 @@ def sidp_plan(num_layers, steps, ranks=0, rank=0):
     n = ctypes.c_int32(cap)
     _check(_lib.sidp_plan(num_layers, steps, ranks, rank, buf, ctypes.byref(n)), "sidp_plan")
     return [(PLAN_OPS[buf[3 * i]], buf[3 * i + 1], buf[3 * i + 2]) for i in range(n.value)]
+
+
+def sidp_linear_plan(m, n, k, epilogue, num_cus=256):
+    """The launch a projection gets (host only): kernel (0 registers, 1
+    LDS-staged weights), waves and rows per workgroup, split-K count,
+    workgroups and bytes of partials."""
+    out = [ctypes.c_int32() for _ in range(5)]
+    ws = ctypes.c_uint64()
+    _check(_lib.sidp_linear_plan(m, n, k, epilogue, num_cus, *[ctypes.byref(o) for o in out], ctypes.byref(ws)),
+           "sidp_linear_plan")
+    names = ("kernel", "waves", "rows", "splits", "workgroups")
+    return dict({nm: o.value for nm, o in zip(names, out)}, ws_bytes=ws.value)
 
 
 def sidp_peak_shift_plan(num_layers, ranks, rank):

@@ -33,6 +33,15 @@ size_t packed_bytes(int n, int k);
 bool gemm_fits(int m, int n_cols_packed, int k);  // within the kernels' 32-bit buffer offsets
 int gemm_splits(int M, int n_cols_packed, int K, int num_cus);
 size_t gemm_ws_bytes(int M, int n_cols_packed, int K, int num_cus);
+// The launch launch_linear makes for an [m, k] x [n, k]^T projection: kernel
+// 0 = k_gemm (weights into registers), 1 = k_gemm_lw (256-row workgroups,
+// weight tiles staged in LDS); waves and rows per workgroup; split-K count;
+// workgroups launched; bytes of fp32 partials (0 without a split).
+struct GemmPlan {
+  int kernel, waves, rows, splits, workgroups;
+  size_t ws_bytes;
+};
+GemmPlan plan_linear(int m, int n, int k, int epilogue, int num_cus);
 hipError_t launch_pack_linear(const void* w, int n, int k, void* packed, hipStream_t s);
 // W_q [nq, k], W_k and W_v [nkv, k] packed as the one stacked matrix [nq + 2 nkv, k]
 hipError_t launch_pack_qkv(const void* wq, const void* wk, const void* wv, int nq, int nkv, int k, void* packed,

@@ -667,6 +667,50 @@ static hipError_t launch_epi(const GemmArgs& a, hipStream_t s, int wide = 0) {
   return launch_mf<4, EPI, P>(a, s);
 }
 
+// Without a split, past 64 rows, a 7- or 8-wave workgroup (128 rows x 448 or
+// 512 columns) stages each activation tile once for all its column groups, so
+// a wave issues fewer loads per k step (the projections pay per load
+// instruction). The width is chosen by the waves a CU runs to finish the grid:
+// 4-wave workgroups go two to a CU (rounds of 8 waves), 7- and 8-wave ones one
+// (rounds of 7 or 8), and a wide width is a candidate only while it gives at
+// least 0.8 workgroups per CU (fewer would leave CUs idle that the model
+// counts as busy); ties go to the wider one. A 70B-shaped gate/up (896 column
+// groups) gets 7 waves at 256 rows, exactly 256 workgroups; a 924-group one 8.
+// Returns 4, 7 or 8.
+static int unsplit_width(int m, int NG, int num_cus) {
+  int wide = 4;
+  if (m > 64) {
+    const int64_t mb = (m + 127) / 128, cus = std::max(1, num_cus);
+    const int64_t n4 = (NG + 3) / 4 * mb, n7 = (NG + 6) / 7 * mb, n8 = (NG + 7) / 8 * mb;
+    int64_t best = (n4 + 2 * cus - 1) / (2 * cus) * 8;
+    if (n7 * 10 >= 8 * cus && (n7 + cus - 1) / cus * 7 <= best) best = (n7 + cus - 1) / cus * 7, wide = 7;
+    if (n8 * 10 >= 8 * cus && (n8 + cus - 1) / cus * 8 <= best) best = (n8 + cus - 1) / cus * 8, wide = 8;
+  }
+  return wide;
+}
+
+GemmPlan plan_linear(int m, int n, int k, int epilogue, int num_cus) {
+  const int ncols = epilogue == SIDP_EPI_SWIGLU ? 2 * round_up(n, 32) : n;
+  const int NG = round_up(ncols, 64) / 64;
+  GemmPlan p;
+  p.splits = gemm_splits(m, ncols, k, num_cus);
+  p.ws_bytes = gemm_ws_bytes(m, ncols, k, num_cus);
+  if (use_lds_weights(m, NG, k, num_cus)) {
+    p.kernel = 1;
+    p.waves = 8;
+    p.rows = kLwRows;
+  } else {
+    p.kernel = 0;
+    p.waves = p.splits == 1 ? unsplit_width(m, NG, num_cus) : kWaves;
+    p.rows = p.waves > kWaves ? 128 : m <= 32 ? 32 : m <= 64 ? 64 : 128;  // launch_epi's MF
+  }
+  const int cols_per_wg = p.kernel == 1 ? 4 : p.waves;  // column groups per workgroup
+  const int tiles = (NG + cols_per_wg - 1) / cols_per_wg;
+  const int mblocks = (m + p.rows - 1) / p.rows;
+  p.workgroups = (tiles * p.splits + 7) / 8 * 8 * mblocks;
+  return p;
+}
+
 hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   GemmArgs a;
   a.x = (const uint16_t*)c.x;
@@ -687,24 +731,10 @@ hipError_t launch_linear(const LinearCall& c, hipStream_t s) {
   if (a.splits > 1 && (size_t)a.splits * a.M * a.NG * 64 * sizeof(float) > c.ws_bytes) return hipErrorInvalidValue;
   const bool fuse_norm = c.norm_out && c.epilogue == SIDP_EPI_RESID && c.residual == c.out;
   if (c.norm_out && !fuse_norm) return hipErrorInvalidValue;
-  // Without a split, past 64 rows, a 7- or 8-wave workgroup (128 rows x 448
-  // or 512 columns) stages each activation tile once for all its column
-  // groups, so a wave issues fewer loads per k step (the projections pay per
-  // load instruction). The width is chosen by the waves a CU runs to finish
-  // the grid: 4-wave workgroups go two to a CU (rounds of 8 waves), 7- and
-  // 8-wave ones one (rounds of 7 or 8), and a wide width is a candidate only
-  // while it gives at least 0.8 workgroups per CU (fewer would leave CUs idle
-  // that the model counts as busy); ties go to the wider one. A 70B-shaped
-  // gate/up (896 column groups) gets 7 waves at 256 rows, exactly 256
-  // workgroups; a 924-group one 8.
-  int wide = use_lds_weights(c.m, a.NG, c.k, c.num_cus) ? -1 : 0;
-  if (wide == 0 && a.splits == 1 && c.m > 64) {
-    const int64_t mb = (c.m + 127) / 128, cus = std::max(1, c.num_cus);
-    const int64_t n4 = (a.NG + 3) / 4 * mb, n7 = (a.NG + 6) / 7 * mb, n8 = (a.NG + 7) / 8 * mb;
-    int64_t best = (n4 + 2 * cus - 1) / (2 * cus) * 8;
-    if (n7 * 10 >= 8 * cus && (n7 + cus - 1) / cus * 7 <= best) best = (n7 + cus - 1) / cus * 7, wide = 7;
-    if (n8 * 10 >= 8 * cus && (n8 + cus - 1) / cus * 8 <= best) best = (n8 + cus - 1) / cus * 8, wide = 8;
-  }
+  // the kernel and width plan_linear describes: -1 the LDS-staged kernel, 7 or
+  // 8 a wide unsplit k_gemm, 0 the 4-wave k_gemm
+  const GemmPlan plan = plan_linear(c.m, c.n, c.k, c.epilogue, c.num_cus);
+  const int wide = plan.kernel == 1 ? -1 : plan.waves > kWaves ? plan.waves : 0;
   hipError_t e;
   if (a.splits == 1) {
     if (c.epilogue == SIDP_EPI_BF16) e = launch_epi<SIDP_EPI_BF16, false>(a, s, wide);

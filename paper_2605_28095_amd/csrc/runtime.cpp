@@ -1056,6 +1056,24 @@ int sidp_linear(sidp_handle* h, const void* x, int32_t m, int32_t k, const void*
   return SIDP_OK;
 }
 
+int sidp_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t num_cus, int32_t* kernel,
+                     int32_t* waves, int32_t* rows_per_workgroup, int32_t* splits, int32_t* workgroups,
+                     uint64_t* ws_bytes) {
+  if (!kernel || !waves || !rows_per_workgroup || !splits || !workgroups || !ws_bytes) return SIDP_EINVAL;
+  if (m < 1 || k < 8 || k % 8 || n < 1 || k > (1 << 24) || n > (1 << 24) || num_cus < 1) return SIDP_EINVAL;
+  if (epilogue < SIDP_EPI_BF16 || epilogue > SIDP_EPI_SWIGLU) return SIDP_EINVAL;
+  const int ncols = epilogue == SIDP_EPI_SWIGLU ? 2 * round_up_i(n, 32) : n;
+  if (!gemm_fits(m, ncols, k)) return SIDP_EINVAL;
+  const GemmPlan p = plan_linear(m, n, k, epilogue, num_cus);
+  *kernel = p.kernel;
+  *waves = p.waves;
+  *rows_per_workgroup = p.rows;
+  *splits = p.splits;
+  *workgroups = p.workgroups;
+  *ws_bytes = p.ws_bytes;
+  return SIDP_OK;
+}
+
 int sidp_slot_mapping(sidp_handle* h, const int32_t* positions, const int32_t* block_tables,
                       int32_t max_blocks_per_seq, int32_t batch, int32_t* slots, void* stream) {
   if (!h || !positions || !block_tables || !slots || batch < 0 || max_blocks_per_seq < 1) return SIDP_EINVAL;

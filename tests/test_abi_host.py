@@ -195,3 +195,46 @@ def test_peak_shift_plan_rejects_bad_arguments():
     assert f(8, 4, 0, None, ctypes.byref(n)) == E
     one = ctypes.c_int32(0)
     assert f(5, 1, 0, None, ctypes.byref(one)) == lib.SIDP_OK and one.value == 0  # nothing to pull
+
+
+# The launches the projections get on a 256-CU MI355X, pinned: the 70B shapes at
+# the benchmark's batch (B=256) and at B=512, where QKV moves to the
+# LDS-staged-weight kernel because the register-fed one would run one unsplit
+# round of 160 workgroups. Each tuple: (m, n, k, epilogue) -> (kernel, waves,
+# rows per workgroup, splits, workgroups).
+LINEAR_PLANS = [
+    ((256, 10240, 8192, 0), (0, 4, 128, 3, 240)),   # QKV
+    ((256, 8192, 8192, 1), (0, 4, 128, 4, 256)),    # O
+    ((256, 28672, 8192, 2), (0, 7, 128, 1, 256)),   # gate/up + SwiGLU, 7-wave workgroups
+    ((256, 8192, 28672, 1), (0, 4, 128, 4, 256)),   # down
+    ((512, 10240, 8192, 0), (1, 8, 256, 3, 240)),   # QKV at 512 rows: LDS-staged weights
+    ((512, 8192, 8192, 1), (0, 4, 128, 2, 256)),
+    ((512, 28672, 8192, 2), (0, 7, 128, 1, 512)),
+    ((384, 10240, 8192, 0), (0, 4, 128, 2, 240)),   # 120 workgroups x 2 splits: no LDS-staged kernel
+    ((16, 10240, 8192, 0), (0, 4, 32, 6, 240)),
+    ((64, 28672, 8192, 2), (0, 4, 64, 1, 224)),
+]
+
+
+@pytest.mark.parametrize("shape,want", LINEAR_PLANS)
+def test_linear_plan_at_model_shapes(shape, want):
+    import paper_2605_28095_amd as sidp
+    m, n, k, epi = shape
+    p = sidp.sidp_linear_plan(m, n, k, epi, 256)
+    assert (p["kernel"], p["waves"], p["rows"], p["splits"], p["workgroups"]) == want
+    ncols = 2 * ((n + 31) // 32 * 32) if epi == 2 else n
+    assert p["ws_bytes"] == (p["splits"] * m * ((ncols + 63) // 64 * 64) * 4 if p["splits"] > 1 else 0)
+
+
+def test_linear_plan_rejects_bad_arguments():
+    import paper_2605_28095_amd as sidp
+    E = sidp.SIDP_EINVAL
+    out = [ctypes.c_int32() for _ in range(5)]
+    ws = ctypes.c_uint64()
+    refs = [ctypes.byref(o) for o in out] + [ctypes.byref(ws)]
+    ok = (256, 8192, 8192, 1, 256)
+    assert sidp.raw_call("sidp_linear_plan", *ok, *refs) == 0
+    for bad in [(0, 8192, 8192, 1, 256), (256, 0, 8192, 1, 256), (256, 8192, 250, 1, 256),
+                (256, 8192, 8192, 3, 256), (256, 8192, 8192, 1, 0), (4, 1 << 21, 1 << 12, 0, 256)]:
+        assert sidp.raw_call("sidp_linear_plan", *bad, *refs) == E, bad
+    assert sidp.raw_call("sidp_linear_plan", *ok, *refs[:-1], None) == E
