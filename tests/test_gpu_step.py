@@ -452,14 +452,17 @@ def test_llama70b_stack80_first10_layers_parity(lib):
         st.close()
 
 
-def test_llama70b_b512_two_layers_parity(lib):
-    """Two layers of the 70B shape at B=512, where the QKV projection runs on
-    the LDS-staged-weight kernel (256-row workgroups, three splits) and the
-    RoPE/KV-append kernel reduces its partials: streamed and resident weights
-    give identical bits, and rows from both 256-row blocks and both 128-row
-    halves of a block (0, 300, 511) match the oracle."""
+@pytest.mark.parametrize("batch,rows", [(512, [0, 300, 511]), (400, [0, 257, 399])])
+def test_llama70b_lds_staged_qkv_two_layers_parity(lib, batch, rows):
+    """Two layers of the 70B shape at 512 and 400 rows, where the QKV
+    projection runs on the LDS-staged-weight kernel (256-row workgroups,
+    three splits; at 400 rows the second workgroup row block is ragged) and
+    the RoPE/KV-append kernel reduces its partials: streamed and resident
+    weights give identical bits, and rows from both 256-row blocks and both
+    128-row halves of a block match the oracle."""
+    assert lib.sidp_linear_plan(batch, 10240, 8192, lib.SIDP_EPI_BF16)["kernel"] == 1
     cfg = synth.get_config("llama70b_stack80", num_layers=2)
-    st = Stack(cfg, batch=512, keep_weights=False, regions=2)
+    st = Stack(cfg, batch=batch, keep_weights=False, regions=2)
     try:
         st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
         st.dec.sync()
@@ -468,11 +471,10 @@ def test_llama70b_b512_two_layers_parity(lib):
         st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
         st.dec.sync()
         assert torch.equal(st.hidden.cpu(), streamed)
-        rows = [0, 300, 511]
         got = streamed.double().numpy()[rows]
         want, _, _, _ = st.run_oracle(rows)
         want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
-        _check_hidden(got, want, want_exact, "70B shape at B=512, 2 layers", tight=False)
+        _check_hidden(got, want, want_exact, f"70B shape at B={batch}, 2 layers", tight=False)
     finally:
         st.close()
 
