@@ -141,8 +141,16 @@ size_t sidp_layer_bytes(const sidp_config *cfg);
 /* Registers caller-owned device memory: `pool` holds num_layers blobs
  * (pool_bytes >= L * sidp_layer_bytes), `slots` holds 2 slots
  * (slots_bytes >= 2 * sidp_layer_bytes; may be NULL/0 if only
- * SIDP_RESIDENT steps will run). Both must be 256-byte aligned. */
-int sidp_pool_init(sidp_handle *h, void *pool, size_t pool_bytes, void *slots, size_t slots_bytes);
+ * SIDP_RESIDENT steps will run). Both must be 256-byte aligned.
+ * With `layers` (host array of n_layers = num_layers entries, device
+ * pointers as in sidp_pool_load_layer) it also puts every layer's weights
+ * into the pool: the owner registering its layers (§4.1), equivalent to one
+ * sidp_pool_load_layer call per layer on `stream`; with layers NULL,
+ * n_layers must be 0 and layers are loaded later, one call each.
+ * SIDP_EINVAL for bad memory, n_layers not matching, or a layer's missing
+ * pointer (layers before it are loaded). */
+int sidp_pool_init(sidp_handle *h, void *pool, size_t pool_bytes, void *slots, size_t slots_bytes,
+                   const sidp_layer_weights *layers, int32_t n_layers, void *stream);
 /* Packs one layer's weights (device pointers, layout above) into its pool
  * blob: norm gains, QKV bias, then the QKV, O, interleaved gate/up and down
  * matrices re-laid into the GEMM's fragment order. Asynchronous on `stream`;

@@ -106,7 +106,7 @@ _sigs = {
     "sidp_create": (ctypes.c_int, [ctypes.POINTER(sidp_config), ctypes.POINTER(_P)]),
     "sidp_destroy": (ctypes.c_int, [_P]),
     "sidp_layer_bytes": (_Z, [ctypes.POINTER(sidp_config)]),
-    "sidp_pool_init": (ctypes.c_int, [_P, _P, _Z, _P, _Z]),
+    "sidp_pool_init": (ctypes.c_int, [_P, _P, _Z, _P, _Z, ctypes.POINTER(sidp_layer_weights), _I, _P]),
     "sidp_pool_load_layer": (ctypes.c_int, [_P, _I, ctypes.POINTER(sidp_layer_weights), _P]),
     "sidp_kv_alloc": (ctypes.c_int, [_I, _PI, _I, _I, _I, ctypes.c_uint64, _I, _PI]),
     "sidp_kv_region_bytes": (_Z, [ctypes.POINTER(sidp_config), _I]),
@@ -202,13 +202,24 @@ def sidp_layer_bytes(config):
     return _lib.sidp_layer_bytes(ctypes.byref(config))
 
 
-def sidp_pool_init(h, pool, pool_bytes, slots, slots_bytes):
-    _check(_lib.sidp_pool_init(h, _ptr(pool), pool_bytes, _ptr(slots), slots_bytes), "sidp_pool_init")
+def _layer_struct(weights):
+    return sidp_layer_weights(**{k: _ptr(v) for k, v in weights.items() if k in dict(sidp_layer_weights._fields_)})
+
+
+def sidp_pool_init(h, pool, pool_bytes, slots, slots_bytes, layers=None, stream=None):
+    """Registers the pool and slots; with `layers` (one mapping name -> device
+    tensor per layer) also loads every layer into the pool."""
+    arr, n = None, 0
+    if layers is not None:
+        n = len(layers)
+        arr = (sidp_layer_weights * max(n, 1))(*[_layer_struct(w) for w in layers])
+    _check(_lib.sidp_pool_init(h, _ptr(pool), pool_bytes, _ptr(slots), slots_bytes, arr, n, _stream(stream)),
+           "sidp_pool_init")
 
 
 def sidp_pool_load_layer(h, layer, weights, stream=None):
     """weights: mapping name -> device tensor (names of sidp_layer_weights)."""
-    w = sidp_layer_weights(**{k: _ptr(v) for k, v in weights.items() if k in dict(sidp_layer_weights._fields_)})
+    w = _layer_struct(weights)
     _check(_lib.sidp_pool_load_layer(h, layer, ctypes.byref(w), _stream(stream)), "sidp_pool_load_layer")
 
 

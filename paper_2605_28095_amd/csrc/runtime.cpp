@@ -372,9 +372,11 @@ int sidp_destroy(sidp_handle* h) {
   return SIDP_OK;
 }
 
-int sidp_pool_init(sidp_handle* h, void* pool, size_t pool_bytes, void* slots, size_t slots_bytes) {
+int sidp_pool_init(sidp_handle* h, void* pool, size_t pool_bytes, void* slots, size_t slots_bytes,
+                   const sidp_layer_weights* layers, int32_t n_layers, void* stream) {
   if (!h) return SIDP_EINVAL;
   if (h->poisoned) return SIDP_ESTATE;
+  if (layers ? n_layers != h->cfg.num_layers : n_layers != 0) return SIDP_EINVAL;
   const size_t lb = h->blob.total;
   if (!pool || pool_bytes < lb * (size_t)h->cfg.num_layers || ((uintptr_t)pool % kAlign)) return SIDP_EINVAL;
   if (slots && (slots_bytes < lb * kSlots || ((uintptr_t)slots % kAlign))) return SIDP_EINVAL;
@@ -385,6 +387,10 @@ int sidp_pool_init(sidp_handle* h, void* pool, size_t pool_bytes, void* slots, s
   h->loaded.assign(h->cfg.num_layers, 0);
   h->ring_started = false;
   h->ring_g = 0;
+  for (int l = 0; layers && l < n_layers; l++) {
+    const int e = sidp_pool_load_layer(h, l, &layers[l], stream);
+    if (e != SIDP_OK) return e;
+  }
   return SIDP_OK;
 }
 

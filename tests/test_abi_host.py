@@ -115,6 +115,7 @@ def test_null_handle_calls_are_rejected():
     assert sidp.raw_call("sidp_plan", 0, 1, 0, 0, None, None) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_set_fill_tiles", None, 25, 0, 0, 1) == sidp.SIDP_EINVAL
     assert sidp.raw_call("sidp_debug_inject_hip_error", None, 1) == sidp.SIDP_EINVAL
+    assert sidp.raw_call("sidp_pool_init", None, None, 0, None, 0, None, 0, None) == sidp.SIDP_EINVAL
 
 
 def test_key_block_layout_helpers():

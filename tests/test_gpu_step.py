@@ -303,6 +303,34 @@ def test_reload_layer_between_streamed_steps_bitexact(lib):
         st.close()
 
 
+def test_pool_init_with_layers_equals_per_layer_loads(lib):
+    """Registering the pool together with every layer's weights fills it with
+    the same bytes as one sidp_pool_load_layer call per layer, and the call
+    checks the layer count and each layer's pointers."""
+    cfg = _small_stack_cfg(num_layers=3)
+    st = Stack(cfg, gains="random", regions=1)  # loads its layers one call each
+    other = lib.WaSDecoder(cfg, st.batch, st.max_seq_len, st.nblk, 1, device="cuda")
+    try:
+        ws = [synth.layer_weights(cfg, l, seed=0, device="cuda", gains="random") for l in range(3)]
+        d = other
+        lib.sidp_pool_init(d.h, d.pool, d.pool.numel(), d.slots, d.slots.numel(), layers=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(d.pool, st.dec.pool)
+        E = lib.SIDP_EINVAL
+        for bad in (ws[:2], ws + ws[:1]):  # layer count must match
+            arr = (lib.sidp_layer_weights * len(bad))(*[lib._layer_struct(w) for w in bad])
+            assert lib.raw_call("sidp_pool_init", d.h, d.pool.data_ptr(), d.pool.numel(), None, 0, arr, len(bad),
+                                None) == E
+        assert lib.raw_call("sidp_pool_init", d.h, d.pool.data_ptr(), d.pool.numel(), None, 0, None, 3, None) == E
+        broken = [dict(w) for w in ws]
+        del broken[2]["w_down"]
+        arr = (lib.sidp_layer_weights * 3)(*[lib._layer_struct(w) for w in broken])
+        assert lib.raw_call("sidp_pool_init", d.h, d.pool.data_ptr(), d.pool.numel(), None, 0, arr, 3, None) == E
+    finally:
+        other.close()
+        st.close()
+
+
 def test_steps_on_changing_compute_streams_bitexact(lib):
     """Consecutive steps issued on different compute streams (and copy
     streams) are ordered by the library: the result equals the same steps on
