@@ -413,13 +413,15 @@ int sidp_linear(sidp_handle *h, const void *x, int32_t m, int32_t k, const void 
  * same split of K); m <= 4096. Allocates nothing: the split-K partials go to
  * a scratch array of SIDP_NOALLOC_SCRATCH_BYTES that the library's code
  * object holds in each device's memory from module load until the process
- * ends (32 MiB: the most any split needs on a 256-CU MI355X). SIDP_EINVAL
+ * ends (64 MiB: the most any split needs on a 256-CU MI355X, where the
+ * splits x row blocks x column blocks of a launch stay within the CU count
+ * and a workgroup's fp32 partial block is at most 256 x 256). SIDP_EINVAL
  * for bad arguments and when this shape's partials would outgrow the scratch
  * (possible only on a device with more CUs); SIDP_EHIP if the runtime fails.
  * Every call on a device shares that device's scratch, and nothing in it must
  * start at zero (each split writes its partials before they are summed);
  * calls that overlap in time on one device (on different streams) race. */
-#define SIDP_NOALLOC_SCRATCH_BYTES (32u << 20)
+#define SIDP_NOALLOC_SCRATCH_BYTES (64u << 20)
 int sidp_linear_noalloc(const void *x, int32_t m, int32_t k, const void *packed, int32_t n, int32_t epilogue,
                         const void *bias, const float *residual, void *out, void *stream);
 

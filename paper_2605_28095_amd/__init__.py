@@ -38,6 +38,8 @@ SIDP_EPI_BF16 = 0
 SIDP_EPI_RESID = 1
 SIDP_EPI_SWIGLU = 2
 
+SIDP_NOALLOC_SCRATCH_BYTES = 64 << 20  # sidp_linear_noalloc's per-device scratch
+
 PLAN_OPS = {0: "fill_a", 1: "fill_b", 2: "wait_fill", 3: "attn", 4: "mid", 5: "proj", 6: "done", 7: "wait_done",
             8: "wait_mid", 9: "local"}
 

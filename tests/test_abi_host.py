@@ -227,6 +227,26 @@ def test_linear_plan_at_model_shapes(shape, want):
     assert p["ws_bytes"] == (p["splits"] * m * ((ncols + 63) // 64 * 64) * 4 if p["splits"] > 1 else 0)
 
 
+def test_noalloc_scratch_holds_every_split_on_256_cus():
+    """The scratch of sidp_linear_noalloc is as large as the header says and
+    holds the split-K partials of every projection plan on a 256-CU MI355X up
+    to its 4096-row limit, both kernels included."""
+    import paper_2605_28095_amd as sidp
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "sidp.h")).read()
+    m = re.search(r"#define SIDP_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == sidp.SIDP_NOALLOC_SCRATCH_BYTES
+    most, kernels = 0, set()
+    for rows in [1, 40, 128, 129, 200, 256, 257, 384, 400, 512, 640, 768, 1024, 2048, 4096]:
+        for n in [64, 520, 1000, 1280, 4096, 8192, 10240, 14336, 28672, 32768]:
+            for k in [256, 1024, 8192, 28672]:
+                for epi in (0, 2):
+                    p = sidp.sidp_linear_plan(rows, n, k, epi, 256)
+                    assert p["ws_bytes"] <= sidp.SIDP_NOALLOC_SCRATCH_BYTES, (rows, n, k, epi, p)
+                    most = max(most, p["ws_bytes"])
+                    kernels.add(p["kernel"])
+    assert kernels == {0, 1} and most > 32 << 20
+
+
 def test_linear_plan_rejects_bad_arguments():
     import paper_2605_28095_amd as sidp
     E = sidp.SIDP_EINVAL

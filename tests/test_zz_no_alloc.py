@@ -39,10 +39,11 @@ def test_noalloc_projection_matches_handle_projection_twice(lib):
     h = lib.sidp_create(lib.make_config(cfg, 512, 64))
     try:
         s = torch.cuda.current_stream().cuda_stream
-        # first call: the O projection at the benchmark batch (4 splits, 32 MiB of
-        # partials, the whole scratch); second: a smaller ragged one with bias
-        cases = [(256, 8192, 8192, lib.SIDP_EPI_RESID, 1), (40, 1000, 520, lib.SIDP_EPI_BF16, 2),
-                 (96, 688, 256, lib.SIDP_EPI_SWIGLU, 3)]
+        # first call: QKV with bias at 512 rows (the LDS-staged kernel, 3 splits,
+        # 60 MiB of partials); then the O projection at 256 rows (4 splits, 32 MiB)
+        # and smaller ragged ones, each starting on what the one before left
+        cases = [(512, 10240, 8192, lib.SIDP_EPI_BF16, 4), (256, 8192, 8192, lib.SIDP_EPI_RESID, 1),
+                 (40, 1000, 520, lib.SIDP_EPI_BF16, 2), (96, 688, 256, lib.SIDP_EPI_SWIGLU, 3)]
         for m, n, k, epi, seed in cases:
             print(f"noalloc case m={m} n={n} k={k} epilogue={epi}", flush=True)
             x, pk, bias, resid, ref, got = _case(lib, h, m, n, k, epi, seed)
