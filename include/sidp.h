@@ -138,6 +138,11 @@ int sidp_destroy(sidp_handle *h);
  * Bytes of one packed layer blob: the pool stride and the size of one slot.
  * Returns 0 for an invalid config. */
 size_t sidp_layer_bytes(const sidp_config *cfg);
+/* Bytes the pool needs (num_layers blobs, §4.1) and the two cache slots
+ * need (§4.2), i.e. num_layers and 2 times sidp_layer_bytes; 0 for an
+ * invalid config. Host only. */
+size_t sidp_pool_bytes(const sidp_config *cfg);
+size_t sidp_slot_bytes(const sidp_config *cfg);
 /* Registers caller-owned device memory: `pool` holds num_layers blobs
  * (pool_bytes >= L * sidp_layer_bytes), `slots` holds 2 slots
  * (slots_bytes >= 2 * sidp_layer_bytes; may be NULL/0 if only

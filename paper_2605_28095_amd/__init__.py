@@ -48,6 +48,7 @@ SIDP_POOL_FFN = 1
 
 EXPORTED = [
     "sidp_strerror", "sidp_last_hip_error", "sidp_create", "sidp_destroy", "sidp_layer_bytes",
+    "sidp_pool_bytes", "sidp_slot_bytes",
     "sidp_pool_init", "sidp_pool_load_layer", "sidp_kv_alloc", "sidp_kv_region_bytes", "sidp_kv_attach",
     "sidp_decode_step", "sidp_sync", "sidp_plan", "sidp_peak_shift_plan", "sidp_rmsnorm", "sidp_packed_bytes", "sidp_pack_linear",
     "sidp_pack_gate_up", "sidp_linear", "sidp_slot_mapping", "sidp_rope_append", "sidp_attention", "sidp_copy",
@@ -108,6 +109,8 @@ _sigs = {
     "sidp_create": (ctypes.c_int, [ctypes.POINTER(sidp_config), ctypes.POINTER(_P)]),
     "sidp_destroy": (ctypes.c_int, [_P]),
     "sidp_layer_bytes": (_Z, [ctypes.POINTER(sidp_config)]),
+    "sidp_pool_bytes": (_Z, [ctypes.POINTER(sidp_config)]),
+    "sidp_slot_bytes": (_Z, [ctypes.POINTER(sidp_config)]),
     "sidp_pool_init": (ctypes.c_int, [_P, _P, _Z, _P, _Z, ctypes.POINTER(sidp_layer_weights), _I, _P]),
     "sidp_pool_load_layer": (ctypes.c_int, [_P, _I, ctypes.POINTER(sidp_layer_weights), _P]),
     "sidp_kv_alloc": (ctypes.c_int, [_I, _PI, _I, _I, _I, ctypes.c_uint64, _I, _PI]),
@@ -202,6 +205,14 @@ def sidp_destroy(h):
 
 def sidp_layer_bytes(config):
     return _lib.sidp_layer_bytes(ctypes.byref(config))
+
+
+def sidp_pool_bytes(config):
+    return _lib.sidp_pool_bytes(ctypes.byref(config))
+
+
+def sidp_slot_bytes(config):
+    return _lib.sidp_slot_bytes(ctypes.byref(config))
 
 
 def _layer_struct(weights):

@@ -269,6 +269,16 @@ size_t sidp_layer_bytes(const sidp_config* cfg) {
   return blob_layout(*cfg).total;
 }
 
+size_t sidp_pool_bytes(const sidp_config* cfg) {
+  if (!config_ok(cfg)) return 0;
+  return (size_t)cfg->num_layers * blob_layout(*cfg).total;
+}
+
+size_t sidp_slot_bytes(const sidp_config* cfg) {
+  if (!config_ok(cfg)) return 0;
+  return (size_t)kSlots * blob_layout(*cfg).total;
+}
+
 static void free_device(sidp_handle* h) {
   void* ptrs[] = {h->h, h->qkv, h->q, h->o, h->act, h->ws, h->attn_part, h->attn_plan, h->g_attn_all, h->cas_y, h->rope_cos, h->rope_sin, h->err};
   for (void* p : ptrs)

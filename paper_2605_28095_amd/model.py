@@ -13,6 +13,8 @@ from . import (
     sidp_kv_attach,
     sidp_kv_region_bytes,
     sidp_layer_bytes,
+    sidp_pool_bytes,
+    sidp_slot_bytes,
     sidp_pool_init,
     sidp_pool_load_layer,
     sidp_set_pooling,
@@ -49,9 +51,8 @@ class WaSDecoder:
         self.h = None
         self.h = sidp_create(self.config)
         self.layer_bytes = sidp_layer_bytes(self.config)
-        L = cfg["num_layers"]
-        self.pool = torch.empty(L * self.layer_bytes, dtype=torch.uint8, device=self.device)
-        self.slots = torch.empty(2 * self.layer_bytes, dtype=torch.uint8, device=self.device) if slots else None
+        self.pool = torch.empty(sidp_pool_bytes(self.config), dtype=torch.uint8, device=self.device)
+        self.slots = torch.empty(sidp_slot_bytes(self.config), dtype=torch.uint8, device=self.device) if slots else None
         for t in (self.pool, self.slots):
             if t is not None and t.data_ptr() % 256:
                 raise RuntimeError("device allocation is not 256-byte aligned")

@@ -86,6 +86,8 @@ def test_config_validation_on_host():
     cfg = synth.get_config("llama70b_layer")
     good = sidp.make_config(cfg, 256, 8192)
     lb = sidp.sidp_layer_bytes(good)
+    assert sidp.sidp_pool_bytes(good) == cfg["num_layers"] * lb
+    assert sidp.sidp_slot_bytes(good) == 2 * lb
     # packed projections plus small vectors, all 256-byte aligned
     assert lb % 256 == 0
     assert 2 * synth.layer_param_count(cfg) <= lb < 2 * synth.layer_param_count(cfg) + 64 * 1024
@@ -94,6 +96,7 @@ def test_config_validation_on_host():
         c = sidp.make_config(cfg, 256, 8192)
         setattr(c, field, bad)
         assert sidp.sidp_layer_bytes(c) == 0, field
+        assert sidp.sidp_pool_bytes(c) == 0 and sidp.sidp_slot_bytes(c) == 0, field
     c = sidp.make_config(cfg, 256, 8192)
     c.num_q_heads = 64
     c.num_kv_heads = 2  # group of 32 query heads per KV head is not supported
