@@ -109,7 +109,11 @@ size_t attn_plan_bytes(int max_batch, int max_parts);
 // decode step shares it across its layers). Reads positions, batch,
 // max_blocks, kv.bs, plan, err.
 hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s);
-hipError_t launch_attention(const AttnCall& c, hipStream_t s);
+// With `start`/`stop`, the events take the start time of the attention's
+// first kernel and the end time of its last from those kernels' own
+// dispatches (no marker packets between the kernels of the stream).
+hipError_t launch_attention(const AttnCall& c, hipStream_t s, hipEvent_t start = nullptr,
+                            hipEvent_t stop = nullptr);
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);
 

@@ -22,6 +22,7 @@
 // fp32-like accuracy. Softmax is online in base-2 units; the four waves of an
 // item are merged in LDS; a sequence spanning several partitions is merged
 // by a log-sum-exp combine kernel. Every reduction has a fixed order.
+#include <hip/hip_ext.h>
 #include "common.h"
 #include "internal.h"
 
@@ -515,18 +516,28 @@ hipError_t launch_attn_plan(const AttnCall& c, hipStream_t s) {
 }
 
 template <int D>
-static hipError_t launch_d(const AttnCall& c, int grid, int parts, hipStream_t s) {
+static hipError_t launch_d(const AttnCall& c, int grid, int parts, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
   const size_t lds = (size_t)(128 + 4 * 16 * (D + 1)) * 4;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)k_attn<D>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  k_attn<D><<<grid, 256, lds, s>>>(c);
-  if (parts > 1) k_attn_combine<D><<<dim3(c.hkv, c.batch), 256, 0, s>>>(c);
-  return hipGetLastError();
+  if (!start && !stop) {
+    k_attn<D><<<grid, 256, lds, s>>>(c);
+    if (parts > 1) k_attn_combine<D><<<dim3(c.hkv, c.batch), 256, 0, s>>>(c);
+    return hipGetLastError();
+  }
+  // timed: the events ride on the kernels' own dispatches
+  AttnCall arg = c;
+  void* args[] = {&arg};
+  hipError_t e = hipExtLaunchKernel((const void*)k_attn<D>, dim3(grid), dim3(256), args, lds, s, start,
+                                    parts > 1 ? nullptr : stop, 0);
+  if (e != hipSuccess || parts <= 1) return e;
+  return hipExtLaunchKernel((const void*)k_attn_combine<D>, dim3(c.hkv, c.batch), dim3(256), args, 0, s, nullptr, stop,
+                            0);
 }
 
-hipError_t launch_attention(const AttnCall& call, hipStream_t s) {
+hipError_t launch_attention(const AttnCall& call, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
   if (call.batch <= 0) return hipSuccess;
   AttnCall c = call;
   const int max_tokens = c.max_blocks * c.kv.bs;
@@ -535,8 +546,8 @@ hipError_t launch_attention(const AttnCall& call, hipStream_t s) {
   if (parts > c.max_parts) return hipErrorInvalidValue;
   if (c.hq / c.hkv > 16) return hipErrorInvalidValue;
   const int grid = 2 * c.num_cus;  // persistent: two 4-wave workgroups per CU
-  if (c.d == 128) return launch_d<128>(c, grid, parts, s);
-  if (c.d == 64) return launch_d<64>(c, grid, parts, s);
+  if (c.d == 128) return launch_d<128>(c, grid, parts, s, start, stop);
+  if (c.d == 64) return launch_d<64>(c, grid, parts, s, start, stop);
   return hipErrorInvalidValue;
 }
 

@@ -539,8 +539,9 @@ static LinearCall linear_call(const sidp_handle* h, const void* x, int m, int k,
 // SIDP_TIMING: open a timed interval of kernel class `cls` on stream s.
 static bool timed_class(const sidp_handle* h, int cls) { return h->timing && ((h->timing_mask >> cls) & 1u); }
 
-static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
-  if (!timed_class(h, cls)) return hipSuccess;
+// Takes a (start, stop) event pair for an interval of class `cls` and lists
+// it for sidp_timing_collect.
+static hipError_t time_pair(sidp_handle* h, int cls, hipEvent_t* start, hipEvent_t* stop) {
   hipEvent_t ev[2];
   for (int i = 0; i < 2; i++) {
     if (!h->event_pool.empty()) {
@@ -552,7 +553,16 @@ static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
     }
   }
   h->timed.push_back({cls, ev[0], ev[1]});
-  return hipEventRecord(ev[0], s);
+  *start = ev[0];
+  *stop = ev[1];
+  return hipSuccess;
+}
+
+static hipError_t time_begin(sidp_handle* h, int cls, hipStream_t s) {
+  if (!timed_class(h, cls)) return hipSuccess;
+  hipEvent_t start, stop;
+  hipError_t e = time_pair(h, cls, &start, &stop);
+  return e != hipSuccess ? e : hipEventRecord(start, s);
 }
 static hipError_t time_end(sidp_handle* h, int cls, hipStream_t s) {
   if (!timed_class(h, cls)) return hipSuccess;
@@ -627,8 +637,12 @@ static hipError_t run_attn_half(sidp_handle* h, const uint8_t* wb, int layer, fl
   a.err = h->err;
   a.num_cus = h->num_cus;
   a.plan = h->attn_plan;
-  TIMED(h, SIDP_K_ATTN, s, launch_attention(a, s));
-  return hipSuccess;
+  if (!timed_class(h, SIDP_K_ATTN)) return launch_attention(a, s);
+  // timed through the attention kernels' own dispatches: no marker packets
+  // between the RoPE kernel, the attention and the O projection
+  hipEvent_t start, stop;
+  const hipError_t e = time_pair(h, SIDP_K_ATTN, &start, &stop);
+  return e != hipSuccess ? e : launch_attention(a, s, start, stop);
 }
 
 // The compute stream's waits for the tiles of a slot fill (streamed layers

@@ -121,6 +121,49 @@ def test_streamed_equals_resident_bitexact(lib, batch):
         st.close()
 
 
+@pytest.mark.parametrize("batch,ctx_hi", [(8, 5000), (160, None)])
+def test_timed_steps_equal_untimed_bitexact(lib, batch, ctx_hi):
+    """The timing mode the benchmark measures with changes no bits: streamed
+    steps with only the attention timed (its events taken from the attention
+    kernels' own dispatches) and with every kernel class bracketed give the
+    untimed hidden states and caches, and the intervals count one attention
+    per layer and step, each of positive length. At 8 rows of up to 5000
+    tokens the attention runs in partitions and a combine kernel closes the
+    interval; at 160 rows it runs on whole sequences in one kernel."""
+    over = {"ctx_lo": 3000, "ctx_hi": ctx_hi} if ctx_hi else {}
+    cfg = _small_stack_cfg(num_layers=4, batch=batch, num_phys_blocks=None, **over)
+    st = Stack(cfg, gains="random", regions=2, reserve=2)
+    try:
+        copy = torch.cuda.Stream()
+        outs = {}
+        for name, classes in [("untimed", None), ("attention", ["attention"]), ("all", lib.KERNEL_CLASSES)]:
+            st.reset()
+            flags = lib.SIDP_STREAMED
+            if classes is not None:
+                lib.sidp_timing_select(st.dec.h, classes)
+                flags |= lib.SIDP_TIMING
+            for s in range(2):
+                st.dec.step(st.hidden, st.positions + s, st.bt, flags, copy=copy)
+            st.dec.sync()
+            t = lib.sidp_timing_collect(st.dec.h)
+            outs[name] = (st.hidden.cpu().numpy().copy(), bits(st.dec.k_cache), bits(st.dec.v_cache))
+            if classes is None:
+                continue
+            ms, n = t["attention"]
+            assert n == 2 * cfg["num_layers"] and ms > 0, (name, t["attention"])
+            if name == "attention":
+                assert all(t[c][1] == 0 for c in lib.KERNEL_CLASSES if c != "attention"), t
+            else:
+                assert t["qkv"][1] == n and t["gate_up"][1] == n and t["fill"][1] > 0, t
+        ref = outs["untimed"]
+        assert np.all(np.isfinite(ref[0]))
+        for name, o in outs.items():
+            assert np.array_equal(o[0].view(np.uint32), ref[0].view(np.uint32)), name
+            assert np.array_equal(o[1], ref[1]) and np.array_equal(o[2], ref[2]), name
+    finally:
+        st.close()
+
+
 @pytest.mark.parametrize("mode,ranks,rank", [("ffn", 0, 0), ("layer", 2, 1), ("ffn", 3, 0), ("layer", 1, 0),
                                               ("ffn", 4, 3)])
 def test_pooling_streamed_equals_resident_bitexact(lib, mode, ranks, rank):
