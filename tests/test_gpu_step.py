@@ -550,6 +550,34 @@ def test_llama70b_lds_staged_qkv_two_layers_parity(lib, batch, rows):
         st.close()
 
 
+@pytest.mark.parametrize("batch,rows", [(16, [0, 9, 15]), (64, [0, 37, 63])])
+def test_llama70b_small_batch_two_layers_parity(lib, batch, rows):
+    """Two layers of the 70B shape at the batch sweep's small batches: the
+    projections run 32- and 64-row tiles with K split over the CUs, the
+    attention cuts each sequence (up to 8K tokens) into partitions that the
+    combine kernel merges, and the fill keeps 8 loads per lane in flight.
+    Streamed and resident weights give identical bits, and sampled rows match
+    the oracle."""
+    plan = lib.sidp_linear_plan(batch, 8192, 28672, lib.SIDP_EPI_RESID)
+    assert plan["rows"] == (32 if batch <= 32 else 64) and plan["splits"] > 1
+    cfg = synth.get_config("llama70b_stack80", num_layers=2)
+    st = Stack(cfg, batch=batch, keep_weights=False, regions=2)
+    try:
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_STREAMED, copy=torch.cuda.Stream())
+        st.dec.sync()
+        streamed = st.hidden.cpu().clone()
+        st.reset()
+        st.dec.step(st.hidden, st.positions, st.bt, lib.SIDP_RESIDENT)
+        st.dec.sync()
+        assert torch.equal(st.hidden.cpu(), streamed)
+        got = streamed.double().numpy()[rows]
+        want, _, _, _ = st.run_oracle(rows)
+        want_exact, _, _, _ = st.run_oracle(rows, round_bf16=False)
+        _check_hidden(got, want, want_exact, f"70B shape at B={batch}, 2 layers", tight=False)
+    finally:
+        st.close()
+
+
 def test_llama70b_ffn_only_pooling_owned_layers_sampled_rows(lib):
     """FFN-only pooling on the full-size 70B shape at B=256: four layers,
     layers 1 and 3 owned by this rank (computed from the pool), layers 0 and 2
