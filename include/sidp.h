@@ -222,12 +222,16 @@ int sidp_sync(sidp_handle *h);
  * collect and returns, per kernel class, the summed elapsed milliseconds
  * (ms[SIDP_NUM_KCLASSES], host) and the number of timed launches
  * (launches[SIDP_NUM_KCLASSES], host); then recycles the events. Each pair
- * brackets one layer's launches of that class on the stream they run on. */
+ * brackets one layer's launches of that class on the stream they run on:
+ * the attention's pair takes its times from the attention kernels' own
+ * dispatches, the other classes' are event records around their launches. */
 int sidp_timing_collect(sidp_handle *h, double *ms, int32_t *launches);
 /* Which kernel classes SIDP_TIMING brackets: bit i selects class i
- * (SIDP_K_*); all by default. Each pair of events is a packet on the stream,
- * so a caller timing one class leaves the others unbracketed. SIDP_EINVAL for
- * bits past SIDP_NUM_KCLASSES. */
+ * (SIDP_K_*); all by default. An event record is a packet on the stream
+ * that delays the next kernel by a few microseconds, so a caller timing one
+ * class leaves the others unbracketed (timing the attention alone adds one
+ * such packet per layer, before the attention). SIDP_EINVAL for bits past
+ * SIDP_NUM_KCLASSES. */
 int sidp_timing_select(sidp_handle *h, uint32_t class_mask);
 
 /* ---- pooling ----
