@@ -81,3 +81,32 @@ def test_tail_leg_mode_choice_matches_the_oracle():
     assert got["was_fraction"] == round(want.count(orchestrator.WAS) / len(want), 4)
     assert got["first_cas_iteration"] == want.index(orchestrator.CAS)
     assert got["switches"] == sum(1 for p, q in zip(want, want[1:]) if p != q) == 1
+
+
+def test_traffic_record_is_used_only_while_the_kernel_sources_match(tmp_path, monkeypatch):
+    """bench.py reports the counted HBM traffic of the roofline kernel from a
+    counter summary under profiles/ only while the kernel's sources hash to
+    the value recorded with the counters; after any change to them it reports
+    none. Checked on a copy of the attention kernel's sources with a record
+    written for them."""
+    import hashlib
+    import json
+    import os
+    import shutil
+    sources = ["paper_2605_28095_amd/csrc/k_attn.hip", "paper_2605_28095_amd/csrc/common.h"]
+    root = tmp_path / "repo"
+    (root / "profiles").mkdir(parents=True)
+    h = hashlib.sha256()
+    for src in sources:
+        (root / src).parent.mkdir(parents=True, exist_ok=True)
+        shutil.copy(os.path.join(bench.ROOT, src), root / src)
+        h.update((root / src).read_bytes())
+    rec = {"kernel": "attention", "source_sha256": h.hexdigest(), "sources": sources,
+           "traffic_bytes_per_launch": 4716188566}
+    (root / "profiles" / "attention_x_traffic.md").write_text("# counters\n\n```json\n" + json.dumps(rec) + "\n```\n")
+    monkeypatch.setattr(bench, "ROOT", str(root))
+    assert bench.measured_traffic("attention") == 4716188566
+    assert bench.measured_traffic("gate_up") is None
+    with open(root / sources[0], "a") as f:
+        f.write("\n")
+    assert bench.measured_traffic("attention") is None
