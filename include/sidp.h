@@ -153,7 +153,8 @@ size_t sidp_slot_bytes(const sidp_config *cfg);
  * sidp_pool_load_layer call per layer on `stream`; with layers NULL,
  * n_layers must be 0 and layers are loaded later, one call each.
  * SIDP_EINVAL for bad memory, n_layers not matching, or a layer's missing
- * pointer (layers before it are loaded). */
+ * pointer (layers before it are loaded). Restarts the slot ring; call it
+ * when no decode step is in flight on the handle (after sidp_sync). */
 int sidp_pool_init(sidp_handle *h, void *pool, size_t pool_bytes, void *slots, size_t slots_bytes,
                    const sidp_layer_weights *layers, int32_t n_layers, void *stream);
 /* Packs one layer's weights (device pointers, layout above) into its pool
